@@ -1,0 +1,235 @@
+#!/usr/bin/env python3
+"""Benchmark of the thin-key attention hot path on one MI355X.
+
+One step is one tk_attn_decode call on the Mistral-7B-shaped decode workload
+(batch 16, 32 query / 8 KV heads, context 4096, r 32, d_v 128, bf16): the
+workload the headline metric is quoted on. Inputs are generated on the GPU
+before timing; the timed region rotates over several copies of the caches so
+that the 168 MB step does not run out of the 256 MB last-level cache.
+
+The JSON line reports, besides the contract fields:
+  roofline      achieved algorithmic GB/s of the decode kernel (HIP events on
+                the launch stream, averaged over the timed calls) against
+                8 TB/s, and the HBM traffic per call from rocprofv3 counters
+                when they were taken on the current kernel source;
+  cpu_baseline  the fp64 oracle on the host cores, on a bounded sample of the
+                same workload (not an optimisation target);
+  secondary     the other workloads, each with its own roofline: causal prefill
+                at 8192 tokens (bf16 MFMA), the 131072-token paged decode, the
+                fp8-key decode, and the GPT-2 fp32 prefill.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "thin-key decode-attn HBM GB/s (% peak); prefill-attn TFLOP/s (% MFMA peak)"
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+KERNEL_SOURCES = {"decode": "paper_2603_04427_amd/csrc/decode.hip",
+                  "prefill_bf16": "paper_2603_04427_amd/csrc/prefill_bf16.hip",
+                  "prefill_f32": "paper_2603_04427_amd/csrc/prefill_f32.hip"}
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200, help="timed steps")
+    ap.add_argument("--warmup", type=int, default=10, help="untimed warm-up steps")
+    ap.add_argument("--rotate", type=int, default=8, help="cache copies cycled through in the timed loop")
+    ap.add_argument("--only", default=None, help="time just this workload (e.g. for profiling)")
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget for the oracle's host timing")
+    return ap.parse_args()
+
+
+def source_sha(kind: str) -> str:
+    with open(os.path.join(ROOT, KERNEL_SOURCES[kind]), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def traffic_for(workload: str, kind: str):
+    """HBM bytes per call from committed rocprofv3 counter runs, if taken on this source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f).get(workload)
+    except (OSError, ValueError):
+        return None
+    if not rec or rec.get("source_sha256") != source_sha(kind):
+        return None
+    return rec.get("bytes_per_call")
+
+
+def time_calls(calls, steps: int, warmup: int):
+    """Warm up, then time ``steps`` calls (cycling through ``calls``).
+
+    Returns (wall seconds per step, event seconds per step). The wall clock is
+    bracketed by device synchronisation; the events sit on the launch stream."""
+    import torch
+    n = len(calls)
+    for i in range(warmup):
+        calls[i % n]()
+    torch.cuda.synchronize()
+    st = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(st)
+    for i in range(steps):
+        calls[i % n]()
+    e1.record(st)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / steps
+    ev = e0.elapsed_time(e1) / 1e3 / steps
+    return wall, ev
+
+
+def decode_setup(spec, dev, rotate: int):
+    import torch
+    from paper_2603_04427_amd import prepare_decode, tk_attn_decode_workspace_bytes
+    from synth import make_decode
+
+    d = make_decode(spec, device=dev)
+    d.pop("k_logical"), d.pop("v_logical"), d.pop("k_scale_logical")
+    torch.cuda.empty_cache()
+    ws = torch.zeros(tk_attn_decode_workspace_bytes(spec.batch, spec.h_q, spec.h_kv, spec.ctx, spec.d_v),
+                     dtype=torch.uint8, device=dev)
+    out = torch.empty(spec.batch, spec.h_q, spec.d_v, dtype=torch.bfloat16, device=dev)
+    copies = [(d["k"], d["v"], d["k_scale"])]
+    for _ in range(rotate - 1):
+        copies.append((d["k"].clone(), d["v"].clone(), None if d["k_scale"] is None else d["k_scale"].clone()))
+    calls = [prepare_decode(d["q"], k, v, d["ctx_lens"], max_ctx=spec.ctx, scale=spec.softmax_scale, k_scale=ks,
+                            block_table=d["block_table"], block_size=spec.block_size if spec.paged else 0,
+                            workspace=ws, O=out) for (k, v, ks) in copies]
+    return calls
+
+
+def decode_result(name, spec, calls, steps, warmup):
+    from paper_2603_04427_amd import accounting as acc
+    wall, ev = time_calls(calls, steps, warmup)
+    nbytes = acc.decode_bytes(spec.lens, spec.h_q, spec.h_kv, spec.r, spec.d_v, spec.k_dtype,
+                              spec.blocks_per_seq if spec.paged else None)
+    achieved = nbytes / ev / 1e9
+    traffic = traffic_for(name, "decode")
+    return {
+        "workload": name, "value": round(nbytes / wall / 1e9, 1), "unit": "GB/s",
+        "ms_per_call": round(wall * 1e3, 5),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": acc.HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / acc.HBM_PEAK_GBS, 4), "traffic": traffic,
+                     "algorithmic_bytes": nbytes, "kernel_ms": round(ev * 1e3, 5)},
+    }
+
+
+def prefill_result(name, spec, dev, steps, warmup):
+    import torch
+    from paper_2603_04427_amd import accounting as acc
+    from paper_2603_04427_amd import prepare_prefill
+    from synth import make_prefill
+
+    p = make_prefill(spec, device=dev)
+    call = prepare_prefill(p["q"], p["k"], p["v"], causal=spec.causal, scale=spec.softmax_scale)
+    wall, ev = time_calls([call], steps, warmup)
+    flops = acc.prefill_flops(spec.batch, spec.h_q, spec.seq_q, spec.seq_k, spec.r, spec.d_v, spec.causal)
+    peak = acc.BF16_MFMA_PEAK_TFLOPS if spec.dtype == "bf16" else acc.FP32_MFMA_PEAK_TFLOPS
+    achieved = flops / ev / 1e12
+    kind = "prefill_bf16" if spec.dtype == "bf16" else "prefill_f32"
+    del p, call
+    torch.cuda.empty_cache()
+    return {
+        "workload": name, "value": round(flops / wall / 1e12, 2), "unit": "TFLOP/s",
+        "ms_per_call": round(wall * 1e3, 5), "dtype": spec.dtype,
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": traffic_for(name, kind),
+                     "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5)},
+    }
+
+
+def cpu_baseline(spec, budget_s: float):
+    """The fp64 oracle on the host cores over whole decode steps of the workload,
+    repeated until the time budget is used (at least once)."""
+    import torch
+    from oracle import oracle
+    from paper_2603_04427_amd import accounting as acc
+    from synth import make_decode
+
+    d = make_decode(spec, device="cpu")
+    nbytes = acc.decode_bytes(spec.lens, spec.h_q, spec.h_kv, spec.r, spec.d_v, spec.k_dtype)
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.decode(d["q"], d["k_logical"], d["v_logical"], d["ctx_lens"], scale=spec.softmax_scale,
+                      k_scale=d["k_scale_logical"])
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    del d
+    torch.cuda.empty_cache() if torch.cuda.is_available() else None
+    return {"value": round(nbytes * reps / el / 1e9, 3), "unit": "GB/s", "cores": oracle.max_threads(),
+            "kind": "oracle", "sample": f"{reps} full decode steps of {spec.name} (fp64 C oracle, OpenMP), "
+                                        f"{el:.1f} s", "seconds_per_step": round(el / reps, 4)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py: this build measures one GPU only; the thin-key attention path is not sharded "
+              "across GPUs (see DESIGN.md for how it would shard). Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from synth import WORKLOADS
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    dev = torch.device("cuda", 0)
+    main_name = args.only or "mistral_decode_b16"
+    results = {}
+    order = [main_name] if (args.no_secondary or args.only) else \
+        [main_name] + [n for n in ("mistral_prefill_s8192", "longctx_paged_decode", "fp8key_decode",
+                                   "gpt2_prefill_f32") if n != main_name]
+    for name in order:
+        spec = WORKLOADS[name]
+        print(f"bench: timing {name}", file=sys.stderr, flush=True)
+        if hasattr(spec, "ctx"):
+            big = spec.batch * spec.h_kv * spec.ctx * (spec.r + spec.d_v) * 2 > (1 << 30)
+            calls = decode_setup(spec, dev, 1 if big else args.rotate)
+            steps = args.steps if name == main_name else max(10, args.steps // 10)
+            results[name] = decode_result(name, spec, calls, steps, args.warmup)
+            results[name]["rotate"] = len(calls)
+            del calls
+            torch.cuda.empty_cache()
+        else:
+            steps = args.steps if name == main_name else max(5, args.steps // 20)
+            results[name] = prefill_result(name, spec, dev, steps, min(args.warmup, 3))
+    m = results[main_name]
+    spec = WORKLOADS[main_name]
+    is_decode = hasattr(spec, "ctx")
+    line = {
+        "metric": METRIC, "value": m["value"], "unit": m["unit"], "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": m["ms_per_call"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16" if (not is_decode or spec.k_dtype == "bf16") else "fp8-keys/bf16",
+        "data": "synthetic (seeded N(0,1) draws shaped like the paper's Mistral-7B decode)",
+        "config": ({"workload": main_name, "batch": spec.batch, "h_q": spec.h_q, "h_kv": spec.h_kv,
+                    "ctx": spec.ctx, "r": spec.r, "d_v": spec.d_v, "k_dtype": spec.k_dtype,
+                    "layout": "paged" if spec.paged else "contiguous", "rotate": m.get("rotate")}
+                   if is_decode else
+                   {"workload": main_name, "batch": spec.batch, "h_q": spec.h_q, "h_kv": spec.h_kv,
+                    "seq": spec.seq_q, "r": spec.r, "d_v": spec.d_v, "causal": spec.causal}),
+        "roofline": m["roofline"],
+    }
+    if not args.no_cpu_baseline and is_decode:
+        print("bench: oracle on the host cores", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(spec, args.cpu_seconds)
+    line["secondary"] = [results[n] for n in order if n != main_name]
+    line["device"] = torch.cuda.get_device_name(0)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

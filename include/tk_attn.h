@@ -1,0 +1,137 @@
+/*
+ * tk_attn.h - thin-key attention on AMD Instinct MI355X (gfx950).
+ *
+ * Fused attention forward O = softmax(scale * Q K^T) V in which queries and
+ * keys are "thin" (r entries per head) while values and outputs keep the full
+ * head width d_v: the asymmetric attention of "Thin Keys, Full Values"
+ * (arXiv 2603.04427), Sec. 2.1, Eq. 1-4. Because the attention weights are
+ * scalars, no projection is needed between the r-wide selection and the
+ * d_v-wide value sum (the remark after Eq. 4). Thin keys come either from
+ * training with a small d_select or from factoring a pretrained key projection
+ * (Sec. 2.3, Eq. 6-7, with the factor absorbed into the query projection); both
+ * hand the kernels the same r-wide Q and K.
+ *
+ * Conventions shared by all entry points
+ *  - Every tensor pointer is a DEVICE pointer owned by the caller; the library
+ *    never allocates, frees or synchronises, and keeps no state between calls.
+ *  - Layouts are dense and head-major (innermost dimension last), in elements.
+ *  - Query head h reads KV head g = h / (H_q / H_kv) (grouped-query attention;
+ *    the Mistral-7B setting of Sec. 3, Exp. 8 has 32 query heads over 8 KV heads).
+ *  - scale <= 0 or NaN selects 1/sqrt(r), the 1/sqrt(d_head^QK) of Eq. 4.
+ *  - Accumulation is fp32; bf16 outputs are rounded to nearest-even once.
+ *  - Calls are asynchronous on `stream` (NULL = the null stream). Argument
+ *    checks run on the host before any HIP call and return an error without
+ *    launching anything; device faults surface on the stream as usual.
+ *  - No exception crosses this interface.
+ */
+#ifndef TK_ATTN_H
+#define TK_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TK_OK = 0,
+    TK_ERR_INVALID_ARG = 1,  /* null pointer, bad dimension, inconsistent shapes */
+    TK_ERR_UNSUPPORTED = 2,  /* valid arguments that no kernel here implements   */
+    TK_ERR_WORKSPACE = 3,    /* decode workspace missing or smaller than needed   */
+    TK_ERR_HIP = 4           /* the HIP runtime reported an error at launch       */
+} tk_status;
+
+typedef enum {
+    TK_F32 = 0,
+    TK_BF16 = 1,
+    TK_FP8_E4M3 = 2  /* OCP E4M3FN codes (bias 7, no infinities, max 448) */
+} tk_dtype;
+
+/*
+ * Causal (or full) prefill attention over a whole sequence: the attention core
+ * of Eq. 4 for every query row at once. Prefill is compute-bound (the paper's
+ * prefill roofline appendix); thin keys cut the Q K^T work by r / d_head.
+ *
+ *   Q [batch, H_q,  seq_q, r]     K [batch, H_kv, seq_k, r]
+ *   V [batch, H_kv, seq_k, d_v]   O [batch, H_q,  seq_q, d_v]   (written)
+ *   all of `dtype`: TK_BF16 (bf16 matrix cores, fp32 accumulation) or TK_F32
+ *   (fp32 matrix cores).
+ *
+ * causal != 0: query row i sees keys 0 .. i + (seq_k - seq_q) (bottom-right
+ * alignment, so a chunk of new queries sees the whole cached prefix); requires
+ * seq_q <= seq_k. causal == 0: every row sees all seq_k keys.
+ * Supported: r in {16, 32, 64, 128}; d_v in {64, 128}; H_q % H_kv == 0.
+ * seq_q == 0 or batch == 0 is a no-op; seq_k == 0 with seq_q > 0 is invalid.
+ */
+tk_status tk_attn_prefill(const void* Q, const void* K, const void* V, void* O,
+                          int batch, int H_q, int H_kv, int seq_q, int seq_k, int r, int d_v,
+                          int causal, float scale, tk_dtype dtype, hipStream_t stream);
+
+/*
+ * Bytes of device workspace tk_attn_decode needs for these shapes (split-K
+ * partial results). A pure function of its arguments: no device query.
+ * Returns 0 for invalid shapes.
+ */
+size_t tk_attn_decode_workspace_bytes(int batch, int H_q, int H_kv, int max_ctx, int d_v);
+
+/*
+ * Single-token decode against a thin-key / full-value cache (Sec. 2.4, Eq. 9:
+ * keys occupy r / d_v of the value footprint), with grouped-query sharing, an
+ * optional paged layout and optional fp8 keys (the composition with
+ * quantisation proposed in Sec. 6). Decode is memory-bound (Sec. 4.2, Eq. 10):
+ * every cached K and V byte is read exactly once per call.
+ *
+ *   Q [batch, H_q, r] bf16            O [batch, H_q, d_v] bf16 (written)
+ *   ctx_lens [batch] int32 (device): sequence b attends to its first
+ *       ctx_lens[b] cached tokens (the current token already appended).
+ *       Values are clamped to [0, max_ctx]; 0 writes a zero output row.
+ *   max_ctx (host): an upper bound on ctx_lens; sizes the launch.
+ *   contiguous cache (block_table == NULL):
+ *       K_cache [batch, H_kv, max_ctx, r]   V_cache [batch, H_kv, max_ctx, d_v]
+ *       k_scale [batch, H_kv, max_ctx]
+ *   paged cache (block_table != NULL):
+ *       K_cache [num_blocks, H_kv, block_size, r]
+ *       V_cache [num_blocks, H_kv, block_size, d_v]
+ *       k_scale [num_blocks, H_kv, block_size]
+ *       block_table [batch, max_blocks_per_seq] int32 (device): token t of
+ *       sequence b is slot t % block_size of block block_table[b][t / block_size].
+ *       block_size must be a power of two >= 64 and
+ *       max_ctx <= block_size * max_blocks_per_seq. A table entry outside
+ *       [0, num_blocks) is never dereferenced: that sequence's output is NaN.
+ *   k_dtype: TK_BF16 keys, or TK_FP8_E4M3 key codes (uint8) with one fp32 scale
+ *       per (token, KV head) in k_scale (the key row is code * scale).
+ *       k_scale must be NULL for bf16 keys.
+ *   V_cache is always bf16.
+ *   workspace: device memory of at least
+ *       tk_attn_decode_workspace_bytes(batch, H_q, H_kv, max_ctx, d_v) bytes,
+ *       256-byte aligned. It holds per-split partial results and a small
+ *       leading region of arrival counters: the buffer must be all zero before
+ *       its first use (allocate it zeroed); every completed call leaves the
+ *       counters zero again, so it can be reused without clearing. Calls that
+ *       share one workspace must not run concurrently.
+ * Supported: r in {16, 32, 64, 128}; d_v in {64, 128}; H_q % H_kv == 0.
+ * The split of the context depends only on the shapes, so results are bitwise
+ * reproducible from run to run.
+ */
+tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache, void* O,
+                         int batch, int H_q, int H_kv, const int32_t* ctx_lens, int max_ctx,
+                         int r, int d_v, float scale,
+                         tk_dtype k_dtype, const float* k_scale,
+                         const int32_t* block_table, int block_size, int max_blocks_per_seq,
+                         int num_blocks,
+                         void* workspace, size_t workspace_bytes, hipStream_t stream);
+
+/* A static, human-readable name for a status code. Never NULL. */
+const char* tk_status_str(tk_status status);
+
+/* Library version, major * 10000 + minor * 100 + patch. */
+int tk_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TK_ATTN_H */

@@ -1,0 +1,205 @@
+"""ctypes binding of libtkattn.so, with the C entry points' names.
+
+Argument marshalling only: shapes are read from the tensors, checked for
+consistency, and passed with the tensors' device pointers and torch's current
+HIP stream to the C ABI declared in include/tk_attn.h. Every step of the
+computation runs in the HIP kernels; there is no other code path. If the
+library has not been built, the first call raises instead of falling back.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtkattn.so")
+
+TK_OK, TK_ERR_INVALID_ARG, TK_ERR_UNSUPPORTED, TK_ERR_WORKSPACE, TK_ERR_HIP = 0, 1, 2, 3, 4
+TK_F32, TK_BF16, TK_FP8_E4M3 = 0, 1, 2
+
+# exported functions and their ctypes signatures (kept in step with include/tk_attn.h)
+_vp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+SIGNATURES = {
+    "tk_attn_prefill": ([_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _f, _i, _vp], _i),
+    "tk_attn_decode_workspace_bytes": ([_i, _i, _i, _i, _i], _sz),
+    "tk_attn_decode": ([_vp, _vp, _vp, _vp, _i, _i, _i, _vp, _i, _i, _i, _f, _i, _vp, _vp, _i, _i, _i,
+                        _vp, _sz, _vp], _i),
+    "tk_status_str": ([_i], ctypes.c_char_p),
+    "tk_version": ([], _i),
+}
+
+_lib = None
+
+
+class TkError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {tk_status_str(status)} (status {status})")
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded library (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            raise RuntimeError(f"libtkattn.so not found at {_LIB_PATH}; build it with "
+                               "`python -m paper_2603_04427_amd.build`")
+        L = ctypes.CDLL(_LIB_PATH)
+        for name, (args, res) in SIGNATURES.items():
+            fn = getattr(L, name)
+            fn.argtypes = args
+            fn.restype = res
+        _lib = L
+    return _lib
+
+
+def tk_status_str(status: int) -> str:
+    return lib().tk_status_str(int(status)).decode()
+
+
+def tk_version() -> int:
+    return lib().tk_version()
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream) -> ctypes.c_void_p:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+def _check(t: torch.Tensor, name: str, dtypes, ndim: int):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype} not in {dtypes}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimensions, got {tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+class PreparedCall:
+    """A C entry point with its arguments marshalled once; calling it launches again
+    with the same tensors (for timing loops and graph-free replay)."""
+
+    def __init__(self, name: str, args, keep):
+        self.name = name
+        self.fn = getattr(lib(), name)
+        self.args = args
+        self.keep = keep  # tensors whose memory the pointers refer to
+
+    def __call__(self):
+        st = self.fn(*self.args)
+        if st != TK_OK:
+            raise TkError(st, self.name)
+        return self.keep[-1]
+
+
+def prepare_prefill(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, O: Optional[torch.Tensor] = None,
+                    causal: bool = True, scale: float = 0.0, stream=None) -> PreparedCall:
+    dts = (torch.bfloat16, torch.float32)
+    _check(Q, "Q", dts, 4)
+    _check(K, "K", (Q.dtype,), 4)
+    _check(V, "V", (Q.dtype,), 4)
+    B, Hq, Sq, r = Q.shape
+    _, Hkv, Sk, dv = V.shape
+    if K.shape != (B, Hkv, Sk, r) or V.shape[0] != B:
+        raise ValueError(f"shape mismatch Q{tuple(Q.shape)} K{tuple(K.shape)} V{tuple(V.shape)}")
+    if O is None:
+        O = torch.empty(B, Hq, Sq, dv, dtype=Q.dtype, device=Q.device)
+    _check(O, "O", (Q.dtype,), 4)
+    if O.shape != (B, Hq, Sq, dv):
+        raise ValueError("O has the wrong shape")
+    args = (_ptr(Q), _ptr(K), _ptr(V), _ptr(O), B, Hq, Hkv, Sq, Sk, r, dv, int(bool(causal)), float(scale),
+            TK_BF16 if Q.dtype == torch.bfloat16 else TK_F32, _stream(stream))
+    return PreparedCall("tk_attn_prefill", args, (Q, K, V, O))
+
+
+def tk_attn_prefill(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, O: Optional[torch.Tensor] = None,
+                    causal: bool = True, scale: float = 0.0, stream=None) -> torch.Tensor:
+    """O = softmax(scale Q K^T [causal]) V for Q [B,Hq,Sq,r], K [B,Hkv,Sk,r], V [B,Hkv,Sk,dv]."""
+    return prepare_prefill(Q, K, V, O, causal, scale, stream)()
+
+
+def tk_attn_decode_workspace_bytes(batch: int, H_q: int, H_kv: int, max_ctx: int, d_v: int) -> int:
+    return int(lib().tk_attn_decode_workspace_bytes(batch, H_q, H_kv, max_ctx, d_v))
+
+
+def prepare_decode(Q: torch.Tensor, K_cache: torch.Tensor, V_cache: torch.Tensor, ctx_lens: torch.Tensor,
+                   max_ctx: Optional[int] = None, scale: float = 0.0, k_scale: Optional[torch.Tensor] = None,
+                   block_table: Optional[torch.Tensor] = None, block_size: int = 0,
+                   workspace: Optional[torch.Tensor] = None, O: Optional[torch.Tensor] = None,
+                   stream=None) -> PreparedCall:
+    """One decode step, marshalled. Q [B,Hq,r] bf16; K_cache bf16 or uint8 E4M3 codes (with k_scale fp32);
+    contiguous [B,Hkv,max_ctx,*] or paged [nblk,Hkv,bs,*] with block_table [B, mb] int32."""
+    _check(Q, "Q", (torch.bfloat16,), 3)
+    _check(K_cache, "K_cache", (torch.bfloat16, torch.uint8, torch.float8_e4m3fn), 4)
+    _check(V_cache, "V_cache", (torch.bfloat16,), 4)
+    _check(ctx_lens, "ctx_lens", (torch.int32,), 1)
+    B, Hq, r = Q.shape
+    Hkv, dv = V_cache.shape[1], V_cache.shape[3]
+    fp8 = K_cache.dtype != torch.bfloat16
+    if fp8:
+        if k_scale is None:
+            raise ValueError("fp8 keys need k_scale")
+        _check(k_scale, "k_scale", (torch.float32,), 3)
+        K_cache = K_cache.view(torch.uint8)
+    elif k_scale is not None:
+        raise ValueError("k_scale is only for fp8 keys")
+    if K_cache.shape[1] != Hkv or K_cache.shape[3] != r or K_cache.shape[:3] != V_cache.shape[:3]:
+        raise ValueError(f"cache shapes K{tuple(K_cache.shape)} V{tuple(V_cache.shape)} do not match r={r}")
+    if k_scale is not None and tuple(k_scale.shape) != tuple(K_cache.shape[:3]):
+        raise ValueError("k_scale must be [*, Hkv, tokens]")
+    if ctx_lens.shape[0] != B:
+        raise ValueError("ctx_lens must have one entry per sequence")
+    if block_table is None:
+        if K_cache.shape[0] != B:
+            raise ValueError("contiguous cache must be [B, Hkv, max_ctx, *]")
+        cap = K_cache.shape[2]
+        mb = nblk = 0
+        block_size = 0
+    else:
+        _check(block_table, "block_table", (torch.int32,), 2)
+        if block_table.shape[0] != B:
+            raise ValueError("block_table must be [B, max_blocks_per_seq]")
+        if block_size != K_cache.shape[2]:
+            raise ValueError("block_size must equal the cache's slot dimension")
+        mb = block_table.shape[1]
+        nblk = K_cache.shape[0]
+        cap = mb * block_size
+    if max_ctx is None:
+        max_ctx = cap
+    if max_ctx > cap:
+        raise ValueError("max_ctx exceeds the cache capacity")
+    need = tk_attn_decode_workspace_bytes(B, Hq, Hkv, max_ctx, dv)
+    if workspace is None:
+        workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=Q.device)
+    if workspace.device.type != "cuda":
+        raise ValueError("workspace must be on the GPU")
+    if O is None:
+        O = torch.empty(B, Hq, dv, dtype=torch.bfloat16, device=Q.device)
+    _check(O, "O", (torch.bfloat16,), 3)
+    args = (_ptr(Q), _ptr(K_cache), _ptr(V_cache), _ptr(O), B, Hq, Hkv, _ptr(ctx_lens), int(max_ctx), r, dv,
+            float(scale), TK_FP8_E4M3 if fp8 else TK_BF16, _ptr(k_scale), _ptr(block_table), int(block_size),
+            int(mb), int(nblk), _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
+    return PreparedCall("tk_attn_decode", args, (Q, K_cache, V_cache, ctx_lens, k_scale, block_table, workspace, O))
+
+
+def tk_attn_decode(Q: torch.Tensor, K_cache: torch.Tensor, V_cache: torch.Tensor, ctx_lens: torch.Tensor,
+                   max_ctx: Optional[int] = None, scale: float = 0.0, k_scale: Optional[torch.Tensor] = None,
+                   block_table: Optional[torch.Tensor] = None, block_size: int = 0,
+                   workspace: Optional[torch.Tensor] = None, O: Optional[torch.Tensor] = None,
+                   stream=None) -> torch.Tensor:
+    """One decode step. Q [B,Hq,r] bf16; K_cache bf16 or uint8 E4M3 codes (with k_scale fp32);
+    contiguous [B,Hkv,max_ctx,*] or paged [nblk,Hkv,bs,*] with block_table [B, mb] int32.
+    A workspace passed in must have been zeroed before its first use (see include/tk_attn.h)."""
+    return prepare_decode(Q, K_cache, V_cache, ctx_lens, max_ctx, scale, k_scale, block_table, block_size,
+                          workspace, O, stream)()

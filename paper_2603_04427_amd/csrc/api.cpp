@@ -1,0 +1,138 @@
+// C-ABI entry points of libtkattn: argument validation (pure host code, no HIP
+// call until it passes), decode planning and kernel dispatch.
+#include <math.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "tk_attn.h"
+#include "tk_internal.hpp"
+
+namespace {
+
+bool supported_r(int r) { return r == 16 || r == 32 || r == 64 || r == 128; }
+bool supported_dv(int dv) { return dv == 64 || dv == 128; }
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+float resolve_scale(float scale, int r) { return (scale > 0.f && !isnan(scale)) ? scale : 1.0f / sqrtf((float)r); }
+
+int log2_exact(int x) {
+    int l = 0;
+    while ((1 << l) < x) ++l;
+    return (1 << l) == x ? l : -1;
+}
+
+constexpr long kMaxGrid = 65535;
+
+}  // namespace
+
+extern "C" {
+
+const char* tk_status_str(tk_status s) {
+    switch (s) {
+        case TK_OK: return "ok";
+        case TK_ERR_INVALID_ARG: return "invalid argument";
+        case TK_ERR_UNSUPPORTED: return "unsupported configuration";
+        case TK_ERR_WORKSPACE: return "workspace missing or too small";
+        case TK_ERR_HIP: return "HIP runtime error";
+        default: return "unknown status";
+    }
+}
+
+int tk_version(void) { return 100; }  // 0.1.0
+
+tk_status tk_attn_prefill(const void* Q, const void* K, const void* V, void* O, int batch, int H_q, int H_kv,
+                          int seq_q, int seq_k, int r, int d_v, int causal, float scale, tk_dtype dtype,
+                          hipStream_t stream) {
+    if (batch < 0 || H_q <= 0 || H_kv <= 0 || seq_q < 0 || seq_k < 0 || r <= 0 || d_v <= 0)
+        return TK_ERR_INVALID_ARG;
+    if (H_q % H_kv != 0) return TK_ERR_INVALID_ARG;
+    if (dtype != TK_F32 && dtype != TK_BF16) return dtype == TK_FP8_E4M3 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
+    if (causal && seq_q > seq_k) return TK_ERR_INVALID_ARG;
+    if (batch == 0 || seq_q == 0) return TK_OK;
+    if (seq_k == 0) return TK_ERR_INVALID_ARG;
+    if (!Q || !K || !V || !O) return TK_ERR_INVALID_ARG;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return TK_ERR_INVALID_ARG;
+    if (!supported_r(r) || !supported_dv(d_v)) return TK_ERR_UNSUPPORTED;
+    const int G = H_q / H_kv;
+    const int hpw = (G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1);
+    const long bm = 32L * (4 / hpw);
+    if ((seq_q + bm - 1) / bm > 0x7fffffffL || (long)H_kv * (G / hpw) > kMaxGrid || batch > kMaxGrid)
+        return TK_ERR_UNSUPPORTED;
+
+    tk::PrefillParams p{};
+    p.q = Q;
+    p.k = K;
+    p.v = V;
+    p.o = O;
+    p.B = batch;
+    p.Hq = H_q;
+    p.Hkv = H_kv;
+    p.G = G;
+    p.Sq = seq_q;
+    p.Sk = seq_k;
+    p.causal = causal ? 1 : 0;
+    p.qscale = resolve_scale(scale, r) * tk::kLog2e;
+    return dtype == TK_BF16 ? tk::launch_prefill_bf16(p, r, d_v, stream) : tk::launch_prefill_f32(p, r, d_v, stream);
+}
+
+size_t tk_attn_decode_workspace_bytes(int batch, int H_q, int H_kv, int max_ctx, int d_v) {
+    if (batch <= 0 || H_q <= 0 || H_kv <= 0 || H_q % H_kv != 0 || max_ctx < 0 || d_v <= 0) return 0;
+    return tk::plan_decode(batch, H_q, H_kv, max_ctx, d_v).ws_bytes;
+}
+
+tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache, void* O, int batch, int H_q,
+                         int H_kv, const int32_t* ctx_lens, int max_ctx, int r, int d_v, float scale,
+                         tk_dtype k_dtype, const float* k_scale, const int32_t* block_table, int block_size,
+                         int max_blocks_per_seq, int num_blocks, void* workspace, size_t workspace_bytes,
+                         hipStream_t stream) {
+    if (batch < 0 || H_q <= 0 || H_kv <= 0 || max_ctx < 0 || r <= 0 || d_v <= 0) return TK_ERR_INVALID_ARG;
+    if (H_q % H_kv != 0) return TK_ERR_INVALID_ARG;
+    if (k_dtype != TK_BF16 && k_dtype != TK_FP8_E4M3) return k_dtype == TK_F32 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
+    const bool fp8 = k_dtype == TK_FP8_E4M3;
+    if (fp8 != (k_scale != nullptr)) return TK_ERR_INVALID_ARG;  // scales iff fp8 keys
+    const bool paged = block_table != nullptr;
+    int bs_log2 = 0;
+    if (paged) {
+        if (block_size <= 0 || max_blocks_per_seq <= 0 || num_blocks <= 0) return TK_ERR_INVALID_ARG;
+        if ((long)block_size * max_blocks_per_seq < max_ctx) return TK_ERR_INVALID_ARG;
+        bs_log2 = log2_exact(block_size);
+        if (bs_log2 < 0 || block_size < 64) return TK_ERR_UNSUPPORTED;
+    } else if (block_size != 0 || max_blocks_per_seq != 0 || num_blocks != 0) {
+        return TK_ERR_INVALID_ARG;  // layout arguments without a table
+    }
+    if (batch == 0) return TK_OK;
+    if (!Q || !K_cache || !V_cache || !O || !ctx_lens) return TK_ERR_INVALID_ARG;
+    if (!aligned16(Q) || !aligned16(K_cache) || !aligned16(V_cache) || !aligned16(O)) return TK_ERR_INVALID_ARG;
+    if (!supported_r(r) || !supported_dv(d_v)) return TK_ERR_UNSUPPORTED;
+    if (batch > kMaxGrid) return TK_ERR_UNSUPPORTED;
+
+    const tk::DecodePlan pl = tk::plan_decode(batch, H_q, H_kv, max_ctx, d_v);
+    if ((long)H_kv * (H_q / H_kv / pl.heads_per_group) > kMaxGrid || pl.n_split > 0x7fffffff)
+        return TK_ERR_UNSUPPORTED;
+    if (!workspace || workspace_bytes < pl.ws_bytes || ((uintptr_t)workspace & 255u)) return TK_ERR_WORKSPACE;
+
+    tk::DecodeParams p{};
+    p.q = (const uint16_t*)Q;
+    p.k = (const uint8_t*)K_cache;
+    p.k_scale = k_scale;
+    p.v = (const uint16_t*)V_cache;
+    p.ctx_lens = ctx_lens;
+    p.block_table = block_table;
+    p.counters = (unsigned*)workspace;
+    p.ws = (float*)((char*)workspace + pl.counter_bytes);
+    p.o = (uint16_t*)O;
+    p.B = batch;
+    p.Hq = H_q;
+    p.Hkv = H_kv;
+    p.G = H_q / H_kv;
+    p.max_ctx = max_ctx;
+    p.bs_log2 = bs_log2;
+    p.mb = paged ? max_blocks_per_seq : 0;
+    p.num_blocks = paged ? num_blocks : 0;
+    p.n_split = pl.n_split;
+    p.split_len = pl.split_len;
+    p.qscale = resolve_scale(scale, r) * tk::kLog2e;
+    return tk::launch_decode(p, r, d_v, pl.heads_per_group, fp8, paged, stream);
+}
+
+}  // extern "C"

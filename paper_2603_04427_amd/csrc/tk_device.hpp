@@ -1,0 +1,104 @@
+// Device helpers shared by the gfx950 kernels: bf16 unpacking and packing,
+// OCP E4M3 decoding through the hardware converter, and wavefront reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace tk {
+
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(16 * sizeof(float)))) float f32x16;
+typedef __attribute__((__vector_size__(8 * sizeof(short)))) short bf16x8;
+typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2;
+
+// bf16 pair packed in one dword -> two floats (exact).
+__device__ __forceinline__ float bf16lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Two floats -> packed bf16 pair, round to nearest even (v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    const f32x2_t x = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(x, bf16x2_t));
+}
+
+// sum of a packed bf16 pair, accumulated in fp32 (v_dot2c_f32_bf16 against (1, 1))
+__device__ __forceinline__ float add_bf16_pair(uint32_t pair, float acc) {
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const uint32_t ones = 0x3f803f80u;
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, pair),
+                                           __builtin_bit_cast(bf16x2_t, ones), acc, false);
+}
+
+// Four OCP E4M3 codes in one dword -> four floats (exact), gfx950 converter.
+__device__ __forceinline__ void e4m3x4(uint32_t w, float& a, float& b, float& c, float& d) {
+    f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
+    f32x2 hi = __builtin_amdgcn_cvt_pk_f32_fp8(w, true);
+    a = lo[0];
+    b = lo[1];
+    c = hi[0];
+    d = hi[1];
+}
+
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ---------------------------------------------------------------- cross-lane
+// DPP lane permutations inside a row of 16 lanes.
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, true));
+}
+constexpr int kQuadXor1 = 0xB1;    // quad_perm [1,0,3,2]
+constexpr int kQuadXor2 = 0x4E;    // quad_perm [2,3,0,1]
+constexpr int kRowHalfMirror = 0x141;
+constexpr int kRowMirror = 0x140;
+
+// Sum / max over aligned groups of N lanes (N a power of two <= 64); every lane
+// of the group receives the result.
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+    if constexpr (N >= 2) x += dpp<kQuadXor1>(x);
+    if constexpr (N >= 4) x += dpp<kQuadXor2>(x);
+    if constexpr (N >= 8) x += dpp<kRowHalfMirror>(x);
+    if constexpr (N >= 16) x += dpp<kRowMirror>(x);
+    if constexpr (N >= 32) x += __shfl_xor(x, 16);
+    if constexpr (N >= 64) x += __shfl_xor(x, 32);
+    return x;
+}
+
+template <int N>
+__device__ __forceinline__ float group_max(float x) {
+    if constexpr (N >= 2) x = fmaxf(x, dpp<kQuadXor1>(x));
+    if constexpr (N >= 4) x = fmaxf(x, dpp<kQuadXor2>(x));
+    if constexpr (N >= 8) x = fmaxf(x, dpp<kRowHalfMirror>(x));
+    if constexpr (N >= 16) x = fmaxf(x, dpp<kRowMirror>(x));
+    if constexpr (N >= 32) x = fmaxf(x, __shfl_xor(x, 16));
+    if constexpr (N >= 64) x = fmaxf(x, __shfl_xor(x, 32));
+    return x;
+}
+
+// Max / sum across lanes with the same (lane % STRIDE), STRIDE a power of two:
+// reduces over the lane bits at and above log2(STRIDE).
+template <int STRIDE>
+__device__ __forceinline__ float strided_max(float x) {
+#pragma unroll
+    for (int m = STRIDE; m < 64; m <<= 1) x = fmaxf(x, __shfl_xor(x, m));
+    return x;
+}
+template <int STRIDE>
+__device__ __forceinline__ float strided_sum(float x) {
+#pragma unroll
+    for (int m = STRIDE; m < 64; m <<= 1) x += __shfl_xor(x, m);
+    return x;
+}
+
+// Make this wave's LDS writes visible to its other lanes before they read.
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+}  // namespace tk

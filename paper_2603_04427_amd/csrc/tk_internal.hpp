@@ -1,0 +1,58 @@
+// Internal interface between the C-ABI layer (api.cpp) and the kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "tk_attn.h"
+
+namespace tk {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Decode: one 256-thread workgroup per (split, KV head x head group, sequence).
+struct DecodeParams {
+    const uint16_t* q;          // [B, Hq, R] bf16
+    const uint8_t* k;           // key rows: bf16 (2R bytes) or E4M3 codes (R bytes)
+    const float* k_scale;       // per key row (fp8 only)
+    const uint16_t* v;          // value rows, DV bf16
+    const int32_t* ctx_lens;    // [B]
+    const int32_t* block_table; // [B, mb] or null
+    float* ws;                  // partials [B, Hq, n_split, DV + 2]
+    unsigned* counters;         // [B, Hq / HG] arrival counters, zero between calls
+    uint16_t* o;                // [B, Hq, DV] bf16
+    int B, Hq, Hkv, G, max_ctx;
+    int bs_log2, mb, num_blocks;
+    int n_split, split_len;     // split_len: tokens per split, a multiple of 256
+    float qscale;               // softmax scale * log2(e)
+};
+
+struct DecodePlan {
+    int heads_per_group;  // query heads one workgroup serves (divides G, <= 8)
+    int n_split;
+    int split_len;
+    size_t counter_bytes;  // leading counter region of the workspace (256-byte multiple)
+    size_t ws_bytes;
+};
+
+// Pure function of the shapes (no device query).
+DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV);
+
+tk_status launch_decode(const DecodeParams& p, int R, int DV, int HG, bool fp8, bool paged,
+                        hipStream_t stream);
+
+struct PrefillParams {
+    const void* q;   // [B, Hq, Sq, R]
+    const void* k;   // [B, Hkv, Sk, R]
+    const void* v;   // [B, Hkv, Sk, DV]
+    void* o;         // [B, Hq, Sq, DV]
+    int B, Hq, Hkv, G, Sq, Sk;
+    int causal;
+    float qscale;    // softmax scale * log2(e)
+};
+
+tk_status launch_prefill_bf16(const PrefillParams& p, int R, int DV, hipStream_t stream);
+tk_status launch_prefill_f32(const PrefillParams& p, int R, int DV, hipStream_t stream);
+
+}  // namespace tk

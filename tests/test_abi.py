@@ -1,0 +1,105 @@
+"""The C ABI without a GPU: the library loads, exports what include/tk_attn.h
+declares, and rejects bad arguments on the host before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2603_04427_amd import binding as tb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "tk_attn.h")
+
+P = ctypes.c_void_p(0x10000)       # aligned, never dereferenced on these paths
+P_ODD = ctypes.c_void_p(0x10008)   # 8-byte aligned only
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tk_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_match_header():
+    names = declared_functions()
+    assert names == sorted(tb.SIGNATURES), names
+    lib = tb.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version():
+    assert tb.tk_status_str(0) == "ok"
+    assert tb.tk_status_str(tb.TK_ERR_WORKSPACE).startswith("workspace")
+    assert tb.tk_status_str(99) == "unknown status"
+    assert tb.tk_version() >= 100
+
+
+def prefill(**kw):
+    a = dict(Q=P, K=P, V=P, O=P, batch=1, H_q=4, H_kv=2, seq_q=8, seq_k=8, r=32, d_v=128, causal=1,
+             scale=0.0, dtype=tb.TK_BF16, stream=None)
+    a.update(kw)
+    return tb.lib().tk_attn_prefill(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H_q=3, H_kv=2), tb.TK_ERR_INVALID_ARG),
+    (dict(H_kv=0), tb.TK_ERR_INVALID_ARG),
+    (dict(batch=-1), tb.TK_ERR_INVALID_ARG),
+    (dict(seq_q=9, seq_k=8), tb.TK_ERR_INVALID_ARG),           # causal needs Sq <= Sk
+    (dict(seq_k=0, causal=0), tb.TK_ERR_INVALID_ARG),
+    (dict(Q=None), tb.TK_ERR_INVALID_ARG),
+    (dict(O=P_ODD), tb.TK_ERR_INVALID_ARG),
+    (dict(r=24), tb.TK_ERR_UNSUPPORTED),
+    (dict(d_v=96), tb.TK_ERR_UNSUPPORTED),
+    (dict(dtype=tb.TK_FP8_E4M3), tb.TK_ERR_UNSUPPORTED),
+    (dict(dtype=7), tb.TK_ERR_INVALID_ARG),
+    (dict(batch=0), tb.TK_OK),                                 # nothing to do, no launch
+    (dict(seq_q=0), tb.TK_OK),
+])
+def test_prefill_validation(kw, status):
+    assert prefill(**kw) == status
+
+
+def decode(**kw):
+    a = dict(Q=P, K=P, V=P, O=P, batch=2, H_q=32, H_kv=8, ctx_lens=P, max_ctx=4096, r=32, d_v=128,
+             scale=0.0, k_dtype=tb.TK_BF16, k_scale=None, block_table=None, block_size=0,
+             max_blocks=0, num_blocks=0, ws=P, ws_bytes=1 << 30, stream=None)
+    a.update(kw)
+    return tb.lib().tk_attn_decode(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H_q=30), tb.TK_ERR_INVALID_ARG),
+    (dict(max_ctx=-1), tb.TK_ERR_INVALID_ARG),
+    (dict(k_dtype=tb.TK_FP8_E4M3), tb.TK_ERR_INVALID_ARG),     # fp8 without scales
+    (dict(k_scale=P), tb.TK_ERR_INVALID_ARG),                  # scales without fp8
+    (dict(k_dtype=tb.TK_F32), tb.TK_ERR_UNSUPPORTED),
+    (dict(block_size=256), tb.TK_ERR_INVALID_ARG),             # layout args without a table
+    (dict(block_table=P, block_size=0, max_blocks=16, num_blocks=32), tb.TK_ERR_INVALID_ARG),
+    (dict(block_table=P, block_size=256, max_blocks=8, num_blocks=32), tb.TK_ERR_INVALID_ARG),  # 2048 < ctx
+    (dict(block_table=P, block_size=32, max_blocks=128, num_blocks=256), tb.TK_ERR_UNSUPPORTED),
+    (dict(block_table=P, block_size=96, max_blocks=64, num_blocks=256), tb.TK_ERR_UNSUPPORTED),
+    (dict(ctx_lens=None), tb.TK_ERR_INVALID_ARG),
+    (dict(V=P_ODD), tb.TK_ERR_INVALID_ARG),
+    (dict(r=48), tb.TK_ERR_UNSUPPORTED),
+    (dict(d_v=256), tb.TK_ERR_UNSUPPORTED),
+    (dict(ws=None), tb.TK_ERR_WORKSPACE),
+    (dict(ws_bytes=16), tb.TK_ERR_WORKSPACE),
+    (dict(ws=ctypes.c_void_p(0x10010)), tb.TK_ERR_WORKSPACE),  # not 256-byte aligned
+    (dict(batch=0), tb.TK_OK),
+])
+def test_decode_validation(kw, status):
+    assert decode(**kw) == status
+
+
+def test_workspace_query_is_pure_and_sized():
+    ws = tb.tk_attn_decode_workspace_bytes
+    a = ws(16, 32, 8, 4096, 128)
+    assert a == ws(16, 32, 8, 4096, 128) > 0
+    counters = 512                                            # 16 x 8 arrival counters (4 B), padded to 256
+    assert (a - counters) % (16 * 32 * 130 * 4) == 0          # + [B, Hq, n_split, d_v + 2] fp32
+    assert ws(16, 30, 8, 4096, 128) == 0 and ws(0, 32, 8, 4096, 128) == 0
+    assert ws(8, 32, 8, 131072, 128) >= 8 * 32 * 130 * 4
+    assert ws(1, 32, 8, 0, 128) == 256 + 32 * 130 * 4         # empty caches: one split

@@ -1,0 +1,158 @@
+"""Decode parity on the GPU: tk_attn_decode against the fp64 oracle on the same
+seeded inputs, at small sweep sizes (every output), at the full workload sizes
+in the launch configuration the benchmark times (every output of the
+batch-16 Mistral step; sampled sequences of the long-context and fp8 steps),
+plus invariants that must hold at any size."""
+import pytest
+import torch
+
+from gpu_cases import decode_on_gpu, decode_oracle, device, gate, say
+from synth import WORKLOADS, DecodeSpec, make_decode, with_shape
+
+pytestmark = pytest.mark.gpu
+
+BASE = DecodeSpec("sweep", 100, 3, 8, 2, 320, 32, 128)
+
+
+def run_case(spec, structured=False, batches=None, on_gpu_inputs=False):
+    dev = device()
+    d = make_decode(spec, device=dev if on_gpu_inputs else "cpu", structured=structured)
+    say(f"decode {spec}")
+    out = decode_on_gpu(d, spec, dev)
+    torch.cuda.synchronize()
+    ref = decode_oracle(d, spec, batches)
+    if batches is not None:
+        out = out[torch.tensor(batches, device=out.device)]
+    return out, ref
+
+
+@pytest.mark.parametrize("r", [16, 32, 64, 128])
+@pytest.mark.parametrize("dv", [64, 128])
+@pytest.mark.parametrize("fp8", [False, True])
+@pytest.mark.parametrize("paged", [False, True])
+def test_sweep_shapes(r, dv, fp8, paged):
+    spec = with_shape(BASE, config_id=100 + r + dv, r=r, d_v=dv, k_dtype="fp8" if fp8 else "bf16",
+                      paged=paged, block_size=64, ctx=320, ctx_lens=(320, 1, 200))
+    for structured in (False, True):
+        out, ref = run_case(spec, structured)
+        gate(out, ref, "fp8" if fp8 else "bf16", f"{spec} structured={structured}")
+
+
+@pytest.mark.parametrize("G", [1, 2, 3, 4, 8, 16])
+def test_gqa_group_sizes(G):
+    spec = with_shape(BASE, config_id=200 + G, h_q=2 * G, h_kv=2, ctx=513, ctx_lens=(513, 77, 64))
+    out, ref = run_case(spec, structured=True)
+    gate(out, ref, "bf16", f"G={G}")
+
+
+@pytest.mark.parametrize("lens", [(0, 0, 0), (1, 0, 2), (63, 64, 65), (255, 256, 257), (1000, 999, 1)])
+def test_ragged_and_empty_contexts(lens):
+    spec = with_shape(BASE, config_id=300, ctx=1000, ctx_lens=lens)
+    out, ref = run_case(spec, structured=True)
+    gate(out, ref, "bf16", f"lens={lens}")
+    for b, L in enumerate(lens):
+        if L == 0:
+            assert (out[b] == 0).all()
+
+
+@pytest.mark.parametrize("bs", [64, 128, 256, 512])
+def test_paged_block_sizes(bs):
+    spec = with_shape(BASE, config_id=400 + bs, paged=True, block_size=bs, ctx=1536, ctx_lens=(1536, 700, 1))
+    out, ref = run_case(spec, structured=True)
+    gate(out, ref, "bf16", f"bs={bs}")
+
+
+def test_mistral_decode_b16_full():
+    """Batch 16, 32/8 heads, context 4096, r 32, d_v 128: every output."""
+    spec = WORKLOADS["mistral_decode_b16"]
+    for structured in (False, True):
+        out, ref = run_case(spec, structured)
+        mx, rel = gate(out, ref, "bf16", f"mistral_decode_b16 structured={structured}")
+        say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
+
+
+def test_longctx_paged_decode_full_sampled():
+    """Context 131072 in 256-token pages with a permuted table; oracle on 2 of 8 sequences."""
+    spec = WORKLOADS["longctx_paged_decode"]
+    out, ref = run_case(spec, structured=True, batches=[0, 7], on_gpu_inputs=True)
+    mx, rel = gate(out, ref, "bf16", "longctx_paged_decode")
+    say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
+
+
+def test_fp8key_decode_full_sampled():
+    """Batch 32, context 32768, E4M3 keys with per-token-head scales; oracle on 3 sequences."""
+    spec = WORKLOADS["fp8key_decode"]
+    out, ref = run_case(spec, structured=True, batches=[0, 13, 31], on_gpu_inputs=True)
+    mx, rel = gate(out, ref, "fp8", "fp8key_decode")
+    say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
+
+
+def test_deterministic_and_paged_equals_contiguous():
+    dev = device()
+    spec = with_shape(WORKLOADS["mistral_decode_b16"], batch=4, ctx=4096, ctx_lens=(4096, 3000, 17, 4096))
+    d = make_decode(spec, structured=True)
+    say("decode determinism")
+    a = decode_on_gpu(d, spec, dev)
+    b = decode_on_gpu(d, spec, dev)
+    assert torch.equal(a, b)
+    ps = with_shape(spec, paged=True, block_size=256)
+    dp = make_decode(ps, structured=True)
+    assert torch.equal(dp["k_logical"], d["k_logical"])
+    c = decode_on_gpu(dp, ps, dev)
+    assert torch.equal(a, c)
+
+
+def test_gqa_equals_repeated_heads():
+    """Grouped heads give the same answer as MHA over repeat-interleaved caches."""
+    dev = device()
+    spec = with_shape(BASE, config_id=500, ctx=700, ctx_lens=(700, 300, 5))
+    d = make_decode(spec, structured=True)
+    out = decode_on_gpu(d, spec, dev)
+    G = spec.h_q // spec.h_kv
+    mha = with_shape(spec, h_kv=spec.h_q)
+    dm = dict(d)
+    for key in ("k", "v", "k_logical", "v_logical"):
+        dm[key] = d[key].repeat_interleave(G, dim=1).contiguous()
+    say("decode gqa vs mha")
+    out2 = decode_on_gpu(dm, mha, dev)
+    assert (out.float() - out2.float()).abs().max().item() <= 1e-2
+
+
+def test_workspace_reuse_many_calls():
+    """The split merge's arrival counters reset themselves: 30 calls on one workspace
+    (32 splits per head group), each with new queries, match the oracle and a fresh
+    workspace bitwise, and leave the counters zero."""
+    from oracle import oracle as orc
+    from paper_2603_04427_amd import tk_attn_decode, tk_attn_decode_workspace_bytes
+    from synth import normal, stream_key
+    dev = device()
+    spec = with_shape(BASE, config_id=900, batch=2, h_q=8, h_kv=2, ctx=8192, ctx_lens=(8192, 5000))
+    d = make_decode(spec)
+    k, v, lens = d["k"].to(dev), d["v"].to(dev), d["ctx_lens"].to(dev)
+    ws = torch.zeros(tk_attn_decode_workspace_bytes(2, 8, 2, 8192, 128), dtype=torch.uint8, device=dev)
+    say("decode workspace reuse x30")
+    for i in range(30):
+        q = normal(stream_key(901, i), 2 * 8 * 32).view(2, 8, 32).mul(3.0).to(torch.bfloat16)
+        out = tk_attn_decode(q.to(dev), k, v, lens, workspace=ws)
+        fresh = tk_attn_decode(q.to(dev), k, v, lens)
+        assert torch.equal(out, fresh), i
+        if i % 10 == 0:
+            gate(out, orc.decode(q, d["k"], d["v"], d["ctx_lens"]), "bf16", f"call {i}")
+    torch.cuda.synchronize()
+    assert int(ws[:256].view(torch.int32).abs().sum()) == 0
+
+
+def test_bad_block_table_entry_gives_nan_for_that_sequence():
+    """An out-of-range page index is never dereferenced; only that sequence turns NaN."""
+    dev = device()
+    spec = with_shape(BASE, config_id=950, paged=True, block_size=64, ctx=512, ctx_lens=(512, 512, 300))
+    d = make_decode(spec, structured=True)
+    good = decode_on_gpu(d, spec, dev)
+    d2 = dict(d)
+    t = d["block_table"].clone()
+    t[1, 3] = t.numel() + 5        # beyond the last physical block
+    d2["block_table"] = t
+    say("decode bad block-table entry")
+    out = decode_on_gpu(d2, spec, dev)
+    assert torch.isnan(out[1].float()).all()
+    assert torch.equal(out[0], good[0]) and torch.equal(out[2], good[2])
