@@ -132,7 +132,9 @@ tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache
     p.n_split = pl.n_split;
     p.split_len = pl.split_len;
     p.qscale = resolve_scale(scale, r) * tk::kLog2e;
-    return tk::launch_decode(p, r, d_v, pl.heads_per_group, fp8, paged, stream);
+    // wide keys leave no registers for 8 heads per workgroup: use groups of 4
+    const int hg = (r >= 64 && pl.heads_per_group > 4) ? 4 : pl.heads_per_group;
+    return tk::launch_decode(p, r, d_v, hg, fp8, paged, stream);
 }
 
 }  // extern "C"

@@ -16,7 +16,7 @@
 //    fp8 keys the per-(token, head) scale multiplies the reduced dot product.
 //  * Online softmax per head with a wave-wide running maximum; probabilities go
 //    through a small per-wave LDS table to the lanes that own the value columns.
-//  * The 4 waves of a workgroup merge their (max, sum, output) triples in LDS
+//  * The waves of a workgroup merge their (max, sum, output) triples in LDS
 //    and write one partial per (sequence, head, split). The last workgroup of a
 //    (sequence, head group) to finish - found with an agent-scope counter in the
 //    workspace, which it resets to zero - merges the splits with the log-sum-exp
@@ -26,12 +26,18 @@
 
 #include <math.h>
 
+#ifndef TK_DECODE_TARGET_GROUPS
+#define TK_DECODE_TARGET_GROUPS 256
+#endif
+
 namespace tk {
 
-constexpr int kDecodeThreads = 256;
-constexpr int kDecodeWaves = kDecodeThreads / 64;
-constexpr int kChunk = 64;  // tokens per wave iteration
-constexpr int kMaxSplits = 256;
+#ifndef TK_DECODE_WAVES
+#define TK_DECODE_WAVES 8
+#endif
+constexpr int kDecodeWaves = TK_DECODE_WAVES;  // waves per workgroup, each streaming its own chunks
+constexpr int kDecodeThreads = 64 * kDecodeWaves;
+constexpr int kMaxSplits = 1024;
 
 // Agent-scope relaxed atomic accesses (sc1 on gfx950): coherent across XCDs.
 __device__ __forceinline__ void store_coherent(float* p, float v) {
@@ -40,182 +46,320 @@ __device__ __forceinline__ void store_coherent(float* p, float v) {
 __device__ __forceinline__ float load_coherent(const float* p) {
     return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
+// Raw buffer descriptor over `bytes` bytes at `base` (gfx9 data format word):
+// loads at offsets >= bytes return zero instead of touching memory.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ uint32_t buffer_load4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+}
+// A wave-uniform 32-bit load through the scalar cache (its own counter, so
+// waiting for it does not wait for the vector loads in flight).
+__device__ __forceinline__ int load_uniform(const int32_t* p) {
+    return *(const __attribute__((address_space(4))) int32_t*)p;
+}
+
 // Wait until this thread's outstanding global stores have completed.
 __device__ __forceinline__ void wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-template <int R, int DV, int HG, bool FP8, bool PAGED>
-__global__ __launch_bounds__(kDecodeThreads, 2) void decode_split_kernel(const DecodeParams p) {
-    constexpr int KB = FP8 ? 1 : 2;        // bytes per key element
-    constexpr int ROWB = R * KB;           // bytes per key row
-    constexpr int LPT = ROWB / 16;         // lanes per key row
-    constexpr int EPL = 16 / KB;           // key elements per lane slice
-    constexpr int TPK = 64 / LPT;          // key rows per wave-wide load
-    constexpr int KL = LPT;                // key loads per chunk
-    constexpr int LPV = DV * 2 / 16;       // lanes per value row
-    constexpr int TPV = 64 / LPV;          // value rows per wave-wide load
-    constexpr int VL = LPV;                // value loads per chunk
-    static_assert(LPT >= 1 && LPT <= 16 && LPV >= 8 && LPV <= 16, "unsupported shape");
+template <int R, int DV, int HG, bool FP8, int CH>
+struct DecodeShape {
+    static constexpr int KB = FP8 ? 1 : 2;     // bytes per key element
+    static constexpr int ROWB = R * KB;        // bytes per key row
+    static constexpr int LPT = ROWB / 16;      // lanes per key row (one 16-byte slice each)
+    static constexpr int EPL = 16 / KB;        // key elements per lane slice
+    static constexpr int QW = EPL / 2;         // packed bf16 query dwords per head and lane
+    static constexpr int TPK = 64 / LPT;       // key rows per wave-wide load
+    static constexpr int KL = CH / TPK;        // key loads per chunk
+    static constexpr int LPV = DV * 2 / 16;    // lanes per value row
+    static constexpr int TPV = 64 / LPV;       // value rows per wave-wide load
+    static constexpr int VL = CH / TPV;        // value loads per chunk (even)
+    static_assert(LPT >= 1 && LPT <= 16 && (LPV == 8 || LPV == 16), "unsupported shape");
+    static_assert(KL >= 1 && VL >= 2 && VL % 2 == 0, "chunk too short for this row width");
+};
 
-    __shared__ float p_lds[kDecodeWaves][kChunk * HG];
+// Tokens per wave iteration, and whether the next chunk's loads are issued
+// before the current chunk is processed (two register buffers). Chosen so the
+// buffers fit the 256-register budget of two waves per SIMD: 32-token chunks
+// double-buffered where a chunk would otherwise need too many registers.
+template <int R, int DV, int HG, bool FP8>
+struct DecodeSchedule {
+    static constexpr int kRegs64 = (R * (FP8 ? 1 : 2) / 16) * 4 + (DV / 8) * 4;  // one 64-token buffer
+    static constexpr int kBase = HG * 8 + HG * (FP8 ? 8 : 4) + 2 * HG + 48;
+    static constexpr bool kFits64 = kBase + 2 * kRegs64 + HG * (R * (FP8 ? 1 : 2) / 16) <= 200;
+    static constexpr bool kShort = !kFits64 && 64 / (R * (FP8 ? 1 : 2) / 16) <= 32;
+    static constexpr int CH = kShort ? 32 : 64;
+    static constexpr bool PIPE = kFits64 || kBase + kRegs64 + HG * (R * (FP8 ? 1 : 2) / 16) <= 200;
+};
+
+// One chunk of 64 tokens as this lane holds it.
+template <int R, int DV, int HG, bool FP8, int CH>
+struct Chunk {
+    using S = DecodeShape<R, DV, HG, FP8, CH>;
+    uint4 k[S::KL];
+    float ks[FP8 ? S::KL : 1];
+    uint4 v[S::VL];
+    int nvalid;  // tokens of the chunk inside the context (0: skip, bad page)
+};
+
+// Issues the loads of the CH-token chunk starting at ts through raw buffer
+// descriptors bounded to the rows this call may read (rows at or beyond
+// `avail` come back as zeros from the hardware range check): one 32-bit offset
+// per lane, a wave-uniform base, constant offsets per load, no branches.
+// Returns false (and loads nothing) for a block-table entry outside
+// [0, num_blocks).
+template <int R, int DV, int HG, bool FP8, int CH, bool PAGED>
+__device__ __forceinline__ bool load_chunk(Chunk<R, DV, HG, FP8, CH>& c, const DecodeParams& p, int b, int g, int ts,
+                                           int avail, int lane) {
+    using S = DecodeShape<R, DV, HG, FP8, CH>;
+    const int nrows = avail - ts < CH ? avail - ts : CH;
+    size_t row0;
+    if constexpr (PAGED) {
+        const int blk = load_uniform(p.block_table + (size_t)b * p.mb + (ts >> p.bs_log2));
+        if (blk < 0 || blk >= p.num_blocks) {  // never dereference a bad entry
+            c.nvalid = 0;
+            return false;
+        }
+        row0 = (((size_t)blk * p.Hkv + g) << p.bs_log2) + (ts & ((1 << p.bs_log2) - 1));
+    } else {
+        row0 = ((size_t)b * p.Hkv + g) * p.max_ctx + ts;
+    }
+    c.nvalid = CH;  // refined against the context length when processed
+    const int kgrp = lane / S::LPT, kpart = lane % S::LPT;
+    const int vgrp = lane / S::LPV, vpart = lane % S::LPV;
+    const auto kr = make_rsrc(p.k + row0 * S::ROWB, (uint32_t)(nrows * S::ROWB));
+    const auto vr = make_rsrc(p.v + row0 * DV, (uint32_t)(nrows * DV * 2));
+    const uint32_t koff = (uint32_t)(kgrp * S::ROWB + kpart * 16);
+    const uint32_t voff = (uint32_t)((vgrp * DV + vpart * 8) * 2);
+#pragma unroll
+    for (int j = 0; j < S::KL; ++j) c.k[j] = buffer_load16(kr, koff, j * S::TPK * S::ROWB);
+    if constexpr (FP8) {
+        const auto sr = make_rsrc(p.k_scale + row0, (uint32_t)(nrows * 4));
+#pragma unroll
+        for (int j = 0; j < S::KL; ++j) c.ks[j] = __uint_as_float(buffer_load4(sr, kgrp * 4, j * S::TPK * 4));
+    }
+#pragma unroll
+    for (int j = 0; j < S::VL; ++j) c.v[j] = buffer_load16(vr, voff, j * S::TPV * DV * 2);
+    return true;
+}
+
+// Online-softmax state of one wave: running maximum m (log2 domain, the same
+// in every lane), this lane's share of the normaliser l, and its output columns.
+template <int HG>
+struct WaveState {
+    float m[HG], l[HG], o[HG][8];
+};
+
+// Folds one chunk into the wave's state; rows t >= nvalid of the chunk are
+// outside the context (their scores become -inf and their values zero, since
+// cache memory past the context may hold anything).
+template <int R, int DV, int HG, bool FP8, int CH>
+__device__ __forceinline__ void process_chunk(Chunk<R, DV, HG, FP8, CH>& c, int nvalid, WaveState<HG>& st,
+                                              const uint32_t (&qp)[HG][DecodeShape<R, DV, HG, FP8, CH>::QW],
+                                              float qscale, uint16_t* p16, int lane) {
+    using S = DecodeShape<R, DV, HG, FP8, CH>;
+    const int kgrp = lane / S::LPT, kpart = lane % S::LPT;
+    const int vgrp = lane / S::LPV;
+    c.nvalid = nvalid;
+    if (nvalid < CH) {  // wave-uniform: only the last chunk of a context
+#pragma unroll
+        for (int j = 0; j < S::VL; ++j)
+            if (j * S::TPV + vgrp >= nvalid) c.v[j] = make_uint4(0, 0, 0, 0);
+    }
+
+    // ---- scores (log2 domain) of this lane's key rows for all HG heads
+    float s[S::KL][HG];
+#pragma unroll
+    for (int j = 0; j < S::KL; ++j) {
+        const uint32_t w[4] = {c.k[j].x, c.k[j].y, c.k[j].z, c.k[j].w};
+        uint32_t kb[S::QW];  // key slice as packed bf16 pairs
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (FP8) {
+                kb[2 * i] = e4m3x2_bf16<false>(w[i]);
+                kb[2 * i + 1] = e4m3x2_bf16<true>(w[i]);
+            } else {
+                kb[i] = w[i];
+            }
+        }
+        const bool valid = j * S::TPK + kgrp < c.nvalid;
+        const float sc = FP8 ? qscale * c.ks[FP8 ? j : 0] : qscale;
+#pragma unroll
+        for (int h = 0; h < HG; ++h) {
+            float acc = 0.f;
+#pragma unroll
+            for (int i = 0; i < S::QW; ++i) acc = dot2_bf16(kb[i], qp[h][i], acc);
+            acc = group_sum<S::LPT>(acc);
+            s[j][h] = valid ? acc * sc : -INFINITY;
+        }
+    }
+
+    // ---- chunk maximum per head; rescale the running state when it grows
+#pragma unroll
+    for (int h = 0; h < HG; ++h) {
+        float cm = s[0][h];
+#pragma unroll
+        for (int j = 1; j < S::KL; ++j) cm = fmaxf(cm, s[j][h]);
+        cm = strided_max<S::LPT>(cm);
+        if (cm > st.m[h]) {  // wave-uniform
+            const float alpha = exp2_fast(st.m[h] - cm);
+            st.m[h] = cm;
+            st.l[h] *= alpha;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) st.o[h][e] *= alpha;
+        }
+    }
+
+    // ---- probabilities, rounded to bf16, into the LDS pair table: entry
+    // (pair slot, head) holds the tokens of value loads 2q and 2q+1 that the
+    // same lane will combine
+#pragma unroll
+    for (int j = 0; j < S::KL; ++j) {
+        const int t = j * S::TPK + kgrp;
+        const int jv = t / S::TPV, gv = t % S::TPV;
+        const int slot = ((jv >> 1) * S::TPV + gv) * HG;
+#pragma unroll
+        for (int h = 0; h < HG; ++h) {
+            if (h % S::LPT == kpart) {
+                const float pr = exp2_fast(s[j][h] - st.m[h]);
+                const uint32_t pb = pack_bf16(pr, 0.f) & 0xffffu;
+                st.l[h] += __uint_as_float(pb << 16);
+                p16[(slot + h) * 2 + (jv & 1)] = (uint16_t)pb;
+            }
+        }
+    }
+    wave_lds_sync();
+
+    // ---- value rows: token pairs (t1, t2) of loads 2q, 2q+1 against (p1, p2) with dot2
+    const uint32_t* p32 = (const uint32_t*)p16;
+#pragma unroll
+    for (int q = 0; q < S::VL / 2; ++q) {
+        uint32_t pp[HG];
+#pragma unroll
+        for (int h = 0; h < HG; ++h) pp[h] = p32[(q * S::TPV + vgrp) * HG + h];
+        const uint32_t a[4] = {c.v[2 * q].x, c.v[2 * q].y, c.v[2 * q].z, c.v[2 * q].w};
+        const uint32_t bq[4] = {c.v[2 * q + 1].x, c.v[2 * q + 1].y, c.v[2 * q + 1].z, c.v[2 * q + 1].w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const uint32_t lo = lo_halves(a[i], bq[i]);  // column 2i of (t1, t2)
+            const uint32_t hi = hi_halves(a[i], bq[i]);  // column 2i+1
+#pragma unroll
+            for (int h = 0; h < HG; ++h) {
+                st.o[h][2 * i] = dot2_bf16(lo, pp[h], st.o[h][2 * i]);
+                st.o[h][2 * i + 1] = dot2_bf16(hi, pp[h], st.o[h][2 * i + 1]);
+            }
+        }
+    }
+    wave_lds_sync();
+}
+
+template <int R, int DV, int HG, bool FP8, bool PAGED>
+__global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split_kernel(const DecodeParams p) {
+    constexpr int CH = DecodeSchedule<R, DV, HG, FP8>::CH;
+    constexpr bool PIPE = DecodeSchedule<R, DV, HG, FP8>::PIPE;
+    using S = DecodeShape<R, DV, HG, FP8, CH>;
+    constexpr int LPV = S::LPV;
+
+    __shared__ uint32_t p_lds[kDecodeWaves][CH * HG / 2];
     __shared__ float m_lds[kDecodeWaves][HG];
     __shared__ float l_lds[kDecodeWaves][HG];
     __shared__ float o_lds[kDecodeWaves][HG][DV];
 
     const int lane = threadIdx.x & 63;
-    const int wave = threadIdx.x >> 6;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int split = blockIdx.x;
     const int groups_per_kv = p.G / HG;
     const int g = blockIdx.y / groups_per_kv;
     const int h0 = g * p.G + (blockIdx.y % groups_per_kv) * HG;
     const int b = blockIdx.z;
 
-    int L = p.ctx_lens[b];
+    int L = load_uniform(p.ctx_lens + b);
     L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
     const int split_begin = split * p.split_len;
     int split_end = split_begin + p.split_len;
     split_end = split_end < L ? split_end : L;
 
-    // query slice of this lane, pre-multiplied by scale * log2(e)
-    const int kpart = lane % LPT;
-    float qf[HG][EPL];
+    // this lane's query slice as packed bf16 pairs (exact; the scale is applied in fp32)
+    uint32_t qp[HG][S::QW];
+    const int kpart = lane % S::LPT;
 #pragma unroll
     for (int h = 0; h < HG; ++h) {
-        const uint16_t* qrow = p.q + ((size_t)b * p.Hq + h0 + h) * R + kpart * EPL;
+        const uint4* qrow = (const uint4*)(p.q + ((size_t)b * p.Hq + h0 + h) * R + kpart * S::EPL);
 #pragma unroll
-        for (int e = 0; e < EPL; ++e) qf[h][e] = __uint_as_float((uint32_t)qrow[e] << 16) * p.qscale;
+        for (int i = 0; i < S::QW / 4; ++i) {
+            const uint4 w = qrow[i];
+            qp[h][4 * i] = w.x;
+            qp[h][4 * i + 1] = w.y;
+            qp[h][4 * i + 2] = w.z;
+            qp[h][4 * i + 3] = w.w;
+        }
     }
 
-    float m[HG], l[HG], o[HG][8];
+    WaveState<HG> st;
 #pragma unroll
     for (int h = 0; h < HG; ++h) {
-        m[h] = -INFINITY;
-        l[h] = 0.f;
+        st.m[h] = -INFINITY;
+        st.l[h] = 0.f;
 #pragma unroll
-        for (int c = 0; c < 8; ++c) o[h][c] = 0.f;
+        for (int e = 0; e < 8; ++e) st.o[h][e] = 0.f;
     }
     bool bad_block = false;
+    uint16_t* p16 = (uint16_t*)p_lds[wave];
 
-    const int vpart = lane % LPV;
-    float* pw = p_lds[wave];
-
-    for (int ts = split_begin + wave * kChunk; ts < split_end; ts += kDecodeWaves * kChunk) {
-        const int nvalid = split_end - ts < kChunk ? split_end - ts : kChunk;
-        const uint8_t* kbase;
-        const uint16_t* vbase;
-        const float* sbase = nullptr;
-        if constexpr (PAGED) {
-            int blk = p.block_table[(size_t)b * p.mb + (ts >> p.bs_log2)];
-            blk = __builtin_amdgcn_readfirstlane(blk);
-            if (blk < 0 || blk >= p.num_blocks) {  // never dereference a bad entry
-                bad_block = true;
-                continue;
+    // chunks ts, ts + 4 CH, ... of this wave; with PIPE the next chunk's loads
+    // are issued before the current one is processed. For a contiguous cache
+    // the first chunk is requested before the context length has arrived (rows
+    // up to max_ctx are readable); paged caches wait for it, because table
+    // entries past the context need not be valid.
+    constexpr int kStride = kDecodeWaves * CH;
+    int ts = split_begin + wave * CH;
+    int first_avail = split_begin + p.split_len;
+    first_avail = first_avail < p.max_ctx ? first_avail : p.max_ctx;
+    if (PAGED) first_avail = split_end;
+    if (ts < first_avail) {
+        using C = Chunk<R, DV, HG, FP8, CH>;
+        if constexpr (PIPE) {
+            C ca, cb;
+            bool ok_a = load_chunk<R, DV, HG, FP8, CH, PAGED>(ca, p, b, g, ts, first_avail, lane), ok_b = true;
+            while (true) {
+                const bool more_b = ts + kStride < split_end;
+                if (more_b) ok_b = load_chunk<R, DV, HG, FP8, CH, PAGED>(cb, p, b, g, ts + kStride, split_end, lane);
+                if (ts < split_end) {
+                    bad_block |= !ok_a;
+                    if (ok_a) process_chunk<R, DV, HG, FP8, CH>(ca, split_end - ts < CH ? split_end - ts : CH, st, qp,
+                                                                p.qscale, p16, lane);
+                }
+                if (!more_b) break;
+                ts += kStride;
+                const bool more_a = ts + kStride < split_end;
+                if (more_a) ok_a = load_chunk<R, DV, HG, FP8, CH, PAGED>(ca, p, b, g, ts + kStride, split_end, lane);
+                bad_block |= !ok_b;
+                if (ok_b) process_chunk<R, DV, HG, FP8, CH>(cb, split_end - ts < CH ? split_end - ts : CH, st, qp,
+                                                            p.qscale, p16, lane);
+                if (!more_a) break;
+                ts += kStride;
             }
-            const size_t row0 = (((size_t)blk * p.Hkv + g) << p.bs_log2) + (ts & ((1 << p.bs_log2) - 1));
-            kbase = p.k + row0 * ROWB;
-            vbase = p.v + row0 * DV;
-            if constexpr (FP8) sbase = p.k_scale + row0;
         } else {
-            const size_t row0 = ((size_t)b * p.Hkv + g) * p.max_ctx + ts;
-            kbase = p.k + row0 * ROWB;
-            vbase = p.v + row0 * DV;
-            if constexpr (FP8) sbase = p.k_scale + row0;
-        }
-
-        // ---- issue every load of the chunk
-        uint4 kr[KL];
-        float ks[KL];
-#pragma unroll
-        for (int j = 0; j < KL; ++j) {
-            const int t = j * TPK + lane / LPT;
-            kr[j] = t < nvalid ? *(const uint4*)(kbase + (size_t)t * ROWB + kpart * 16) : make_uint4(0, 0, 0, 0);
-            if constexpr (FP8) ks[j] = t < nvalid ? sbase[t] : 0.f;
-        }
-        uint4 vr[VL];
-#pragma unroll
-        for (int j = 0; j < VL; ++j) {
-            const int t = j * TPV + lane / LPV;
-            vr[j] = t < nvalid ? *(const uint4*)(vbase + (size_t)t * DV + vpart * 8) : make_uint4(0, 0, 0, 0);
-        }
-
-        // ---- scores (log2 domain) for this lane's key rows, all HG heads
-        float s[KL][HG];
-#pragma unroll
-        for (int j = 0; j < KL; ++j) {
-            float kf[EPL];
-            const uint32_t w[4] = {kr[j].x, kr[j].y, kr[j].z, kr[j].w};
-            if constexpr (FP8) {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) e4m3x4(w[i], kf[4 * i], kf[4 * i + 1], kf[4 * i + 2], kf[4 * i + 3]);
-            } else {
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    kf[2 * i] = bf16lo(w[i]);
-                    kf[2 * i + 1] = bf16hi(w[i]);
-                }
-            }
-            const bool valid = j * TPK + lane / LPT < nvalid;
-#pragma unroll
-            for (int h = 0; h < HG; ++h) {
-                float acc = 0.f;
-#pragma unroll
-                for (int e = 0; e < EPL; ++e) acc = fmaf(qf[h][e], kf[e], acc);
-                acc = group_sum<LPT>(acc);
-                if constexpr (FP8) acc *= ks[j];
-                s[j][h] = valid ? acc : -INFINITY;
+            int avail = first_avail;
+            for (; ts < avail; ts += kStride, avail = split_end) {
+                C ca;
+                const bool ok = load_chunk<R, DV, HG, FP8, CH, PAGED>(ca, p, b, g, ts, avail, lane);
+                if (ts >= split_end) break;
+                bad_block |= !ok;
+                if (ok) process_chunk<R, DV, HG, FP8, CH>(ca, split_end - ts < CH ? split_end - ts : CH, st, qp,
+                                                          p.qscale, p16, lane);
             }
         }
-
-        // ---- online softmax: chunk maximum per head, rescale the running state
-#pragma unroll
-        for (int h = 0; h < HG; ++h) {
-            float cm = s[0][h];
-#pragma unroll
-            for (int j = 1; j < KL; ++j) cm = fmaxf(cm, s[j][h]);
-            cm = strided_max<LPT>(cm);
-            const float mn = fmaxf(m[h], cm);
-            const float alpha = exp2_fast(m[h] - mn);
-            m[h] = mn;
-            l[h] *= alpha;
-#pragma unroll
-            for (int c = 0; c < 8; ++c) o[h][c] *= alpha;
-        }
-
-        // ---- probabilities: lane (row slice kpart) computes heads h == kpart (mod LPT)
-#pragma unroll
-        for (int j = 0; j < KL; ++j) {
-            const int t = j * TPK + lane / LPT;
-#pragma unroll
-            for (int h = 0; h < HG; ++h) {
-                if (h % LPT == kpart) {
-                    const float pr = exp2_fast(s[j][h] - m[h]);
-                    l[h] += pr;
-                    pw[t * HG + h] = pr;
-                }
-            }
-        }
-        wave_lds_sync();
-
-        // ---- value rows weighted by the probabilities of their token
-#pragma unroll
-        for (int j = 0; j < VL; ++j) {
-            const int t = j * TPV + lane / LPV;
-            float pr[HG];
-#pragma unroll
-            for (int h = 0; h < HG; ++h) pr[h] = pw[t * HG + h];
-            const uint32_t w[4] = {vr[j].x, vr[j].y, vr[j].z, vr[j].w};
-            float vf[8];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                vf[2 * i] = bf16lo(w[i]);
-                vf[2 * i + 1] = bf16hi(w[i]);
-            }
-#pragma unroll
-            for (int h = 0; h < HG; ++h)
-#pragma unroll
-                for (int c = 0; c < 8; ++c) o[h][c] = fmaf(pr[h], vf[c], o[h][c]);
-        }
-        wave_lds_sync();
     }
+    float (&m)[HG] = st.m;
+    float (&l)[HG] = st.l;
+    float (&o)[HG][8] = st.o;
 
     // ---- wave totals: sums over the lanes that saw different rows
 #pragma unroll
@@ -224,7 +368,7 @@ __global__ __launch_bounds__(kDecodeThreads, 2) void decode_split_kernel(const D
 #pragma unroll
         for (int c = 0; c < 8; ++c) o[h][c] = strided_sum<LPV>(o[h][c]);
     }
-    const bool wave_bad = __any(bad_block);
+    const bool wave_bad = bad_block;  // wave-uniform
     if (lane < LPV) {
 #pragma unroll
         for (int h = 0; h < HG; ++h)
@@ -240,9 +384,32 @@ __global__ __launch_bounds__(kDecodeThreads, 2) void decode_split_kernel(const D
     }
     __syncthreads();
 
-    // ---- merge the 4 waves and write this split's partial per head. Partials are
-    // written and read with agent-scope atomic accesses (coherent across the
-    // XCDs' separate L2 caches without an L2 write-back).
+    // ---- merge the waves. With a single split that is the answer: normalise and
+    // write the bf16 rows directly.
+    if (p.n_split == 1) {
+        for (int idx = threadIdx.x; idx < HG * DV; idx += kDecodeThreads) {
+            const int h = idx / DV, c = idx % DV;
+            float M = -INFINITY;
+#pragma unroll
+            for (int w = 0; w < kDecodeWaves; ++w) M = fmaxf(M, m_lds[w][h]);
+            float O = 0.f, Lsum = 0.f;
+            bool bad = false;
+#pragma unroll
+            for (int w = 0; w < kDecodeWaves; ++w) {
+                const float mw = m_lds[w][h];
+                const float e = mw == -INFINITY ? 0.f : exp2_fast(mw - M);
+                O = fmaf(e, o_lds[w][h][c], O);
+                Lsum = fmaf(e, l_lds[w][h], Lsum);
+                bad |= __builtin_isnan(l_lds[w][h]);
+            }
+            const float out = bad ? NAN : (M == -INFINITY ? 0.f : O / Lsum);
+            p.o[((size_t)b * p.Hq + h0 + h) * DV + c] = (uint16_t)(pack_bf16(out, 0.f) & 0xffffu);
+        }
+        return;
+    }
+    // Otherwise write this split's partial per head. Partials are written and
+    // read with agent-scope atomic accesses (coherent across the XCDs' separate
+    // L2 caches without an L2 write-back).
     const int ws_row = DV + 2;
     for (int idx = threadIdx.x; idx < HG * DV; idx += kDecodeThreads) {
         const int h = idx / DV, c = idx % DV;
@@ -269,8 +436,6 @@ __global__ __launch_bounds__(kDecodeThreads, 2) void decode_split_kernel(const D
     // ---- the last workgroup of this (sequence, head group) to finish merges the
     // splits with the log-sum-exp rule and writes the bf16 output rows
     __shared__ int is_last;
-    __shared__ float w_lds[HG][kMaxSplits];   // per-split weights exp2(m_s - M)
-    __shared__ float inv_l_lds[HG];
     wait_stores();  // this thread's partial is visible device-wide
     __syncthreads();
     unsigned* counter = p.counters + (size_t)b * gridDim.y + blockIdx.y;
@@ -279,33 +444,41 @@ __global__ __launch_bounds__(kDecodeThreads, 2) void decode_split_kernel(const D
                   (unsigned)(p.n_split - 1);
     __syncthreads();
     if (!is_last) return;
-    for (int h = wave; h < HG; h += kDecodeWaves) {  // a wave per head: maximum, weights, normaliser
-        const float* base = p.ws + ((size_t)b * p.Hq + h0 + h) * p.n_split * ws_row;
-        float M = -INFINITY;
-        for (int sp = lane; sp < p.n_split; sp += 64) M = fmaxf(M, load_coherent(base + (size_t)sp * ws_row + DV));
-        M = group_max<64>(M);
-        float Lsum = 0.f;
-        bool bad = false;
-        for (int sp = lane; sp < p.n_split; sp += 64) {
-            const float ms = load_coherent(base + (size_t)sp * ws_row + DV);
-            const float ls = load_coherent(base + (size_t)sp * ws_row + DV + 1);
-            const float e = ms == -INFINITY ? 0.f : exp2_fast(ms - M);
-            w_lds[h][sp] = e;
-            Lsum = fmaf(e, ls, Lsum);
-            bad |= __builtin_isnan(ls);
-        }
-        Lsum = group_sum<64>(Lsum);
-        // no visible token -> zeros; a flagged bad block-table entry -> NaN
-        if (lane == 0) inv_l_lds[h] = __any(bad) ? NAN : (M == -INFINITY ? 0.f : 1.f / Lsum);
-    }
-    __syncthreads();
+    // one pass over the splits, 8 at a time (their loads in flight together),
+    // with the running-maximum rule of the online softmax
     for (int idx = threadIdx.x; idx < HG * DV; idx += kDecodeThreads) {
         const int h = idx / DV, c = idx % DV;
-        const float* base = p.ws + ((size_t)b * p.Hq + h0 + h) * p.n_split * ws_row + c;
-        float O = 0.f;
-        for (int sp = 0; sp < p.n_split; ++sp) O = fmaf(w_lds[h][sp], load_coherent(base + (size_t)sp * ws_row), O);
-        const float il = inv_l_lds[h];
-        const float out = __builtin_isnan(il) ? NAN : O * il;
+        const float* base = p.ws + ((size_t)b * p.Hq + h0 + h) * p.n_split * ws_row;
+        float M = -INFINITY, O = 0.f, Lsum = 0.f;
+        bool bad = false;
+        for (int s0 = 0; s0 < p.n_split; s0 += 8) {
+            float ms[8], ls[8], os[8];
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const int sp = s0 + i < p.n_split ? s0 + i : p.n_split - 1;
+                const float* part = base + (size_t)sp * ws_row;
+                ms[i] = load_coherent(part + DV);
+                ls[i] = load_coherent(part + DV + 1);
+                os[i] = load_coherent(part + c);
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                if (s0 + i >= p.n_split) break;
+                bad |= __builtin_isnan(ls[i]);
+                if (ms[i] == -INFINITY) continue;
+                if (ms[i] > M) {
+                    const float alpha = exp2_fast(M - ms[i]);
+                    O *= alpha;
+                    Lsum *= alpha;
+                    M = ms[i];
+                }
+                const float e = exp2_fast(ms[i] - M);
+                O = fmaf(e, os[i], O);
+                Lsum = fmaf(e, ls[i], Lsum);
+            }
+        }
+        // no visible token -> zeros; a flagged bad block-table entry -> NaN
+        const float out = bad ? NAN : (M == -INFINITY ? 0.f : O / Lsum);
         p.o[((size_t)b * p.Hq + h0 + h) * DV + c] = (uint16_t)(pack_bf16(out, 0.f) & 0xffffu);
     }
     if (threadIdx.x == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -321,7 +494,7 @@ DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV) {
     pl.heads_per_group = hg;
     const long pairs = (long)B * Hkv * (G / hg);
     const long quanta = (max_ctx + 255) / 256;  // 256 tokens = one chunk per wave
-    const long target_groups = 1024;             // workgroups to keep 256 CUs streaming
+    const long target_groups = TK_DECODE_TARGET_GROUPS;  // workgroups to keep 256 CUs streaming
     long n_split = (target_groups + pairs - 1) / pairs;
     if (n_split > quanta) n_split = quanta;
     if (n_split > kMaxSplits) n_split = kMaxSplits;
@@ -329,7 +502,8 @@ DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV) {
     long split_quanta = quanta > 0 ? (quanta + n_split - 1) / n_split : 1;
     pl.split_len = (int)(split_quanta * 256);
     pl.n_split = max_ctx > 0 ? (int)((max_ctx + pl.split_len - 1) / pl.split_len) : 1;
-    pl.counter_bytes = ((size_t)B * (Hq / hg) * sizeof(unsigned) + 255) / 256 * 256;
+    // one counter per (sequence, query head) covers any head grouping chosen at launch
+    pl.counter_bytes = ((size_t)B * Hq * sizeof(unsigned) + 255) / 256 * 256;
     pl.ws_bytes = pl.counter_bytes + (size_t)B * Hq * pl.n_split * (DV + 2) * sizeof(float);
     return pl;
 }

@@ -32,6 +32,29 @@ __device__ __forceinline__ float add_bf16_pair(uint32_t pair, float acc) {
                                            __builtin_bit_cast(bf16x2_t, ones), acc, false);
 }
 
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// acc + a.lo * b.lo + a.hi * b.hi for packed bf16 pairs (v_dot2c_f32_bf16; the
+// products are exact in fp32).
+__device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float acc) {
+    return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a), __builtin_bit_cast(bf16x2_t, b), acc,
+                                           false);
+}
+
+// Two OCP E4M3 codes (byte pair 0-1 or 2-3 of w) -> packed bf16 pair, exact.
+template <bool HI>
+__device__ __forceinline__ uint32_t e4m3x2_bf16(uint32_t w) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, HI));
+}
+
+// Byte permute: pairs of 16-bit halves from two dwords.
+__device__ __forceinline__ uint32_t lo_halves(uint32_t a, uint32_t b) {  // (a.lo, b.lo)
+    return __builtin_amdgcn_perm(b, a, 0x05040100u);
+}
+__device__ __forceinline__ uint32_t hi_halves(uint32_t a, uint32_t b) {  // (a.hi, b.hi)
+    return __builtin_amdgcn_perm(b, a, 0x07060302u);
+}
+
 // Four OCP E4M3 codes in one dword -> four floats (exact), gfx950 converter.
 __device__ __forceinline__ void e4m3x4(uint32_t w, float& a, float& b, float& c, float& d) {
     f32x2 lo = __builtin_amdgcn_cvt_pk_f32_fp8(w, false);
@@ -55,6 +78,26 @@ constexpr int kQuadXor2 = 0x4E;    // quad_perm [2,3,0,1]
 constexpr int kRowHalfMirror = 0x141;
 constexpr int kRowMirror = 0x140;
 
+// Exchange across 16- and 32-lane halves (gfx950 v_permlane16_swap /
+// v_permlane32_swap with both operands the same value): r[0] + r[1] is the sum of
+// the lane's value and its partner's (lane ^ 16, resp. lane ^ 32).
+__device__ __forceinline__ float xor16_sum(float x) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor32_sum(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float xor16_max(float x) {
+    auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float xor32_max(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 // Sum / max over aligned groups of N lanes (N a power of two <= 64); every lane
 // of the group receives the result.
 template <int N>
@@ -63,8 +106,8 @@ __device__ __forceinline__ float group_sum(float x) {
     if constexpr (N >= 4) x += dpp<kQuadXor2>(x);
     if constexpr (N >= 8) x += dpp<kRowHalfMirror>(x);
     if constexpr (N >= 16) x += dpp<kRowMirror>(x);
-    if constexpr (N >= 32) x += __shfl_xor(x, 16);
-    if constexpr (N >= 64) x += __shfl_xor(x, 32);
+    if constexpr (N >= 32) x = xor16_sum(x);
+    if constexpr (N >= 64) x = xor32_sum(x);
     return x;
 }
 
@@ -74,23 +117,32 @@ __device__ __forceinline__ float group_max(float x) {
     if constexpr (N >= 4) x = fmaxf(x, dpp<kQuadXor2>(x));
     if constexpr (N >= 8) x = fmaxf(x, dpp<kRowHalfMirror>(x));
     if constexpr (N >= 16) x = fmaxf(x, dpp<kRowMirror>(x));
-    if constexpr (N >= 32) x = fmaxf(x, __shfl_xor(x, 16));
-    if constexpr (N >= 64) x = fmaxf(x, __shfl_xor(x, 32));
+    if constexpr (N >= 32) x = xor16_max(x);
+    if constexpr (N >= 64) x = xor32_max(x);
     return x;
 }
 
 // Max / sum across lanes with the same (lane % STRIDE), STRIDE a power of two:
-// reduces over the lane bits at and above log2(STRIDE).
+// row rotations (DPP row_ror by multiples of STRIDE keep the residue class)
+// inside each 16-lane row, then the 16- and 32-lane half swaps.
 template <int STRIDE>
 __device__ __forceinline__ float strided_max(float x) {
-#pragma unroll
-    for (int m = STRIDE; m < 64; m <<= 1) x = fmaxf(x, __shfl_xor(x, m));
+    if constexpr (STRIDE <= 1) x = fmaxf(x, dpp<0x121>(x));
+    if constexpr (STRIDE <= 2) x = fmaxf(x, dpp<0x122>(x));
+    if constexpr (STRIDE <= 4) x = fmaxf(x, dpp<0x124>(x));
+    if constexpr (STRIDE <= 8) x = fmaxf(x, dpp<0x128>(x));
+    if constexpr (STRIDE <= 16) x = xor16_max(x);
+    if constexpr (STRIDE <= 32) x = xor32_max(x);
     return x;
 }
 template <int STRIDE>
 __device__ __forceinline__ float strided_sum(float x) {
-#pragma unroll
-    for (int m = STRIDE; m < 64; m <<= 1) x += __shfl_xor(x, m);
+    if constexpr (STRIDE <= 1) x += dpp<0x121>(x);
+    if constexpr (STRIDE <= 2) x += dpp<0x122>(x);
+    if constexpr (STRIDE <= 4) x += dpp<0x124>(x);
+    if constexpr (STRIDE <= 8) x += dpp<0x128>(x);
+    if constexpr (STRIDE <= 16) x = xor16_sum(x);
+    if constexpr (STRIDE <= 32) x = xor32_sum(x);
     return x;
 }
 

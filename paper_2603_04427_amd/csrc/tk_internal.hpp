@@ -20,7 +20,7 @@ struct DecodeParams {
     const int32_t* ctx_lens;    // [B]
     const int32_t* block_table; // [B, mb] or null
     float* ws;                  // partials [B, Hq, n_split, DV + 2]
-    unsigned* counters;         // [B, Hq / HG] arrival counters, zero between calls
+    unsigned* counters;         // [B, Hq] arrival counters (first B * Hq / HG used), zero between calls
     uint16_t* o;                // [B, Hq, DV] bf16
     int B, Hq, Hkv, G, max_ctx;
     int bs_log2, mb, num_blocks;
