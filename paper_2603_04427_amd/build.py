@@ -23,6 +23,9 @@ SOURCES = ["api.cpp", "decode.hip", "prefill_bf16.hip", "prefill_f32.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-I" + INCLUDE, "-I" + CSRC,
          # packed fp32 arithmetic stays off: ordinary fp32 code only
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+         # matrix-core accumulators in ordinary VGPRs: the softmax reads the score
+         # tiles directly and the output tiles do not bounce through AGPRs
+         "-mllvm", "-amdgpu-mfma-vgpr-form=1",
          "-Wall", "-Wno-unused-result"]
 
 

@@ -6,26 +6,28 @@
 // cores (v_mfma_f32_32x32x16_bf16); the softmax runs on the vector ALUs.
 //
 // Work decomposition
-//  * A workgroup is 4 waves. Wave w owns 32 query rows of one query head; the
-//    workgroup covers HPW = gcd(G, 4) heads of one KV group and 4 / HPW blocks
-//    of 32 rows, so every K/V tile staged in LDS serves 4 waves.
-//  * Key tiles are 64 keys, double-buffered in LDS: K rows as they are in
-//    memory (r wide, padded by 16 bytes), V transposed to [d_v][64] with the
-//    keys of each 16-key group permuted so that one 16-byte LDS read yields a
-//    lane's operand for the value product. The transpose happens in registers
-//    (byte permutes) between the global load and the LDS store.
-//  * Scores are computed transposed, S^T = K Q^T (keys along the MFMA rows,
-//    queries along the columns): each lane then holds 16 keys of one query per
-//    32-key block, so the row maximum and row sum are in-lane except for one
-//    exchange between the two 32-lane halves, and P^T leaves the accumulators
-//    already in the B-operand layout of O^T = V^T P^T.
-//  * Online softmax in the log2 domain (scale * log2(e) applied in fp32 by one
-//    FMA), with a lazy rescale: the running reference maximum moves only when
-//    some row's maximum exceeds it by more than 8 (a factor of 256), so most
-//    tiles skip rescaling the d_v x 32 accumulator.
-//  * Causal masking is applied only on tiles that cross a wave's diagonal;
-//    tiles entirely above it are skipped; query blocks are issued heaviest
-//    first.
+//  * A workgroup is 4 waves. Each wave owns 64 query rows (two 32-column MFMA
+//    blocks) of one query head; the workgroup covers HPW = gcd(G, 4) heads of
+//    one KV group and 4 / HPW row blocks, so each K/V tile in LDS serves every
+//    wave, and each LDS operand read feeds two MFMAs (LDS bandwidth, about
+//    128 bytes per clock per CU, would otherwise bound the kernel).
+//  * 64-key tiles are double-buffered in LDS and filled straight from global
+//    memory (global_load_lds, 16 bytes per lane), K and V both in their memory
+//    layout with the 16-byte chunks of each row XOR-swizzled so that the
+//    operand reads below are free of bank conflicts.
+//  * Scores are computed transposed, S^T = K Q^T: each lane holds 16 keys of one
+//    query per 32-key block, so the row maximum and row sum stay in-lane except
+//    for one exchange between the two 32-lane halves (v_permlane32_swap), and
+//    P^T leaves the accumulators in the B-operand layout of O^T = V^T P^T. The
+//    V^T operand (8 keys of one column per lane) comes from the untransposed V
+//    tile through the transposing LDS read ds_read_b64_tr_b16.
+//  * Online softmax in the log2 domain (scale * log2(e) applied by one FMA),
+//    with a lazy per-row rescale: a row's reference maximum moves only when its
+//    maximum exceeds it by more than 8 (a factor of 256).
+//  * Causal masking only on tiles that cross a wave's diagonal; tiles above it
+//    are skipped. Workgroups are ordered so that the query blocks of one KV
+//    sequence run together on one XCD (its K/V stays in that XCD's L2),
+//    heaviest (longest causal prefix) first.
 #include "tk_device.hpp"
 #include "tk_internal.hpp"
 
@@ -35,128 +37,174 @@ namespace tk {
 
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kBN = 64;          // keys per tile
-constexpr int kVtStride = kBN + 8;  // bf16 elements per transposed V row (16-byte pad)
+constexpr int kBN = 64;  // keys per tile
+constexpr int kXcds = 8;
 
 __host__ __device__ constexpr int gcd4(int g) { return (g % 4 == 0) ? 4 : (g % 2 == 0 ? 2 : 1); }
 
-// Position of key k (0..63) inside a transposed V row: within each group of 16
-// keys, k = 8a + 4b + c is stored at 8b + 4a + c.
-__device__ __forceinline__ int vt_pos(int k) {
-    const int a = (k >> 3) & 1, bb = (k >> 2) & 1, c = k & 3;
-    return (k & ~15) + 8 * bb + 4 * a + c;
+typedef __attribute__((address_space(3))) void* lds_ptr;
+typedef short v4s __attribute__((ext_vector_type(4)));
+
+// Row swizzle of a tile with W bf16 per row: the 16-byte chunk c of row r is
+// stored at chunk position c ^ swz(r).
+template <int W, bool IS_V>
+__device__ __forceinline__ int swz(int r) {
+    constexpr int CPR = W / 8;                                // 16-byte chunks per row
+    constexpr int RPL = (256 / (2 * W)) > 0 ? 256 / (2 * W) : 1;  // rows per 256-byte bank line
+    if constexpr (IS_V) {
+        return (4 * (r / RPL)) & (CPR - 1);
+    } else {
+        return (r / RPL) & (CPR - 1);
+    }
 }
 
 template <int R, int DV>
 struct Smem {
-    static constexpr int kStride = R + 8;  // bf16 elements per K row in LDS
-    uint16_t k[2][kBN * kStride];
-    uint16_t vt[2][DV * kVtStride];
+    uint16_t k[2][kBN * R];
+    uint16_t v[2][kBN * DV];
 };
 
-template <int R, int DV>
-struct TileRegs {
-    static constexpr int kChunks = kBN * R / 8;                       // 16-byte K chunks per tile
-    static constexpr int kLoads = (kChunks + kThreads - 1) / kThreads;  // per thread
-    uint4 k[kLoads];
-    uint4 v[4];
-};
+// Global->LDS copies of one 64-key K and V tile (global_load_lds, 16 bytes per
+// lane, each wave filling 1 KB of consecutive LDS). Which 16-byte chunk of which
+// row a lane copies does not depend on the tile, so its element offset inside
+// a tile is computed once (TileLanes); a tile then only adds its first row.
+template <int R, int DV, int NT>
+struct TileLanes {
+    static constexpr int KC = kBN * R / 8;   // 16-byte chunks in the K tile
+    static constexpr int VC = kBN * DV / 8;  // ... and in the V tile
+    static constexpr int KL = (KC + NT - 1) / NT;
+    static constexpr int VL = (VC + NT - 1) / NT;
+    uint32_t k_row[KL], k_off[KL];  // tile row and byte offset (in the tile) of each K chunk this lane copies
+    uint32_t v_row[VL], v_off[VL];
 
-template <int R, int DV>
-__device__ __forceinline__ void load_tile(TileRegs<R, DV>& t, const uint16_t* kg, const uint16_t* vg, int base,
-                                          int Sk, int tid) {
-    constexpr int CPR = R / 8;  // 16-byte chunks per K row
+    __device__ __forceinline__ explicit TileLanes(int tid) {
 #pragma unroll
-    for (int i = 0; i < TileRegs<R, DV>::kLoads; ++i) {
-        const int c = tid + i * kThreads;
-        const int row = c / CPR, part = c % CPR;
-        const bool ok = c < TileRegs<R, DV>::kChunks && base + row < Sk;
-        t.k[i] = ok ? *(const uint4*)(kg + (size_t)(base + row) * R + part * 8) : make_uint4(0, 0, 0, 0);
+        for (int i = 0; i < KL; ++i) {
+            const int ci = tid + i * NT;
+            const int r = ci / (R / 8), pos = ci % (R / 8);
+            k_row[i] = r;
+            k_off[i] = (uint32_t)((r * R + (pos ^ swz<R, false>(r)) * 8) * 2);
+        }
+#pragma unroll
+        for (int i = 0; i < VL; ++i) {
+            const int ci = tid + i * NT;
+            const int r = ci / (DV / 8), pos = ci % (DV / 8);
+            v_row[i] = r;
+            v_off[i] = (uint32_t)((r * DV + (pos ^ swz<DV, true>(r)) * 8) * 2);
+        }
     }
-    // V: thread -> (key quad kq, 8-column chunk dc)
-    const int kq = tid & 15, dc = tid >> 4;
+};
+
+// Issue the copies of the tile starting at key `base`. Rows at or past Sk (only
+// in a ragged last tile) re-read row Sk - 1: finite values, masked later.
+template <int R, int DV, int NT>
+__device__ __forceinline__ void load_tile(const TileLanes<R, DV, NT>& tl, uint16_t* ks, uint16_t* vs,
+                                          const uint16_t* kg, const uint16_t* vg, int base, int Sk, int tid) {
+    using T = TileLanes<R, DV, NT>;
+    const int wave_base = tid & ~63;
+    const bool full = base + kBN <= Sk;  // workgroup-uniform
+    const char* kt = (const char*)(kg + (size_t)base * R);
+    const char* vt = (const char*)(vg + (size_t)base * DV);
+    const int last = Sk - base - 1;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int key = base + 4 * kq + i;
-        const bool ok = dc < DV / 8 && key < Sk;
-        t.v[i] = ok ? *(const uint4*)(vg + (size_t)key * DV + dc * 8) : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < T::KL; ++i) {
+        if (T::KC % NT != 0 && wave_base + i * NT >= T::KC) break;
+        uint32_t off = tl.k_off[i];
+        if (!full && (int)tl.k_row[i] > last) off -= (tl.k_row[i] - last) * R * 2;
+        __builtin_amdgcn_global_load_lds((const void*)(kt + off), (lds_ptr)(ks + (wave_base + i * NT) * 8), 16, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < T::VL; ++i) {
+        if (T::VC % NT != 0 && wave_base + i * NT >= T::VC) break;
+        uint32_t off = tl.v_off[i];
+        if (!full && (int)tl.v_row[i] > last) off -= (tl.v_row[i] - last) * DV * 2;
+        __builtin_amdgcn_global_load_lds((const void*)(vt + off), (lds_ptr)(vs + (wave_base + i * NT) * 8), 16, 0, 0);
     }
 }
 
-template <int R, int DV>
-__device__ __forceinline__ void store_tile(const TileRegs<R, DV>& t, uint16_t* ks, uint16_t* vts, int tid) {
-    constexpr int CPR = R / 8;
-    constexpr int KS = Smem<R, DV>::kStride;
+__device__ __forceinline__ void wait_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// exp2(s * c - m) for the 16 keys of k-step q of one 32-query block (accumulator
+// registers 8 (q % 2) .. + 7 of key block q / 2), rounded to a bf16 B operand of
+// O^T = V^T P^T; the row-sum share accumulates the same rounded values.
+__device__ __forceinline__ bf16x8 prob_step(const f32x16 (&s)[2], int q, float m, float c, float& lsum) {
+    uint32_t w[4];
 #pragma unroll
-    for (int i = 0; i < TileRegs<R, DV>::kLoads; ++i) {
-        const int c = tid + i * kThreads;
-        if (c < TileRegs<R, DV>::kChunks) {
-            const int row = c / CPR, part = c % CPR;
-            *(uint4*)(ks + row * KS + part * 8) = t.k[i];
-        }
+    for (int i = 0; i < 4; ++i) {
+        const float p0 = exp2_fast(fmaf(s[q >> 1][8 * (q & 1) + 2 * i], c, -m));
+        const float p1 = exp2_fast(fmaf(s[q >> 1][8 * (q & 1) + 2 * i + 1], c, -m));
+        w[i] = pack_bf16(p0, p1);
+        lsum = add_bf16_pair(w[i], lsum);
     }
-    const int kq = tid & 15, dc = tid >> 4;
-    if (dc < DV / 8) {
-        const int pos = vt_pos(4 * kq);
-        const uint32_t x0[4] = {t.v[0].x, t.v[0].y, t.v[0].z, t.v[0].w};
-        const uint32_t x1[4] = {t.v[1].x, t.v[1].y, t.v[1].z, t.v[1].w};
-        const uint32_t x2[4] = {t.v[2].x, t.v[2].y, t.v[2].z, t.v[2].w};
-        const uint32_t x3[4] = {t.v[3].x, t.v[3].y, t.v[3].z, t.v[3].w};
-#pragma unroll
-        for (int pr = 0; pr < 4; ++pr) {
-            // columns 2pr (low halves) and 2pr+1 (high halves) of the 4 keys
-            uint2 lo, hi;
-            lo.x = __builtin_amdgcn_perm(x1[pr], x0[pr], 0x05040100u);
-            lo.y = __builtin_amdgcn_perm(x3[pr], x2[pr], 0x05040100u);
-            hi.x = __builtin_amdgcn_perm(x1[pr], x0[pr], 0x07060302u);
-            hi.y = __builtin_amdgcn_perm(x3[pr], x2[pr], 0x07060302u);
-            const int d = dc * 8 + 2 * pr;
-            *(uint2*)(vts + d * kVtStride + pos) = lo;
-            *(uint2*)(vts + (d + 1) * kVtStride + pos) = hi;
-        }
-    }
+    return __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+}
+
+// Transposing LDS read of 4 bf16 (ds_read_b64_tr_b16) at byte offset `off`.
+__device__ __forceinline__ v4s tr_read(const uint16_t* tile, uint32_t off) {
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4s*)((const char*)tile + off));
+}
+
+// The V^T operand of k-step q, column block d: lane (half h, column i) needs
+// V[16q + 4h + j][32d + i] (slots 0-3) and V[16q + 8 + 4h + j][32d + i] (slots
+// 4-7), j = 0..3, gathered by two transposing reads in which source lane L of
+// each 16-lane group points at row k0 + L/4, columns d0 + 4 (L % 4) .. + 3.
+// `vbase` is the lane's byte offset for q = 0 (the swizzle term does not depend
+// on q), so k-step q adds 16 q rows.
+template <int DV>
+__device__ __forceinline__ bf16x8 vt_operand(const uint16_t* vs, uint32_t vbase, int q) {
+    const v4s lo = tr_read(vs, vbase + 16 * q * DV * 2);
+    const v4s hi = tr_read(vs, vbase + (16 * q + 8) * DV * 2);
+    bf16x8 a;
+    a[0] = lo[0];
+    a[1] = lo[1];
+    a[2] = lo[2];
+    a[3] = lo[3];
+    a[4] = hi[0];
+    a[5] = hi[1];
+    a[6] = hi[2];
+    a[7] = hi[3];
+    return a;
 }
 
 }  // namespace
 
-template <int R, int DV>
-__global__ __launch_bounds__(kThreads, 2) void prefill_bf16_kernel(const PrefillParams p) {
+// QC: 32-query column blocks per wave (1 or 2); NW: waves per workgroup.
+template <int R, int DV, int QC, int NW>
+__global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_kernel(const PrefillParams p,
+                                                                                     int n_groups) {
     constexpr int KSTEPS = R / 16;  // MFMA K-steps of the score product
     constexpr int DBLK = DV / 32;   // 32-row blocks of O^T
-    constexpr int KS = Smem<R, DV>::kStride;
+    constexpr int NT = 64 * NW;
     __shared__ Smem<R, DV> sm;
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int half = lane >> 5, col = lane & 31;
 
+    // ---- workgroup -> (KV sequence, query block), XCD-aware and heaviest first
     const int HPW = gcd4(p.G);
-    const int RB = 4 / HPW;
-    const int BM = 32 * RB;
+    const int RB = NW / HPW;
+    const int BM = 32 * QC * RB;
     const int nqb = (p.Sq + BM - 1) / BM;
-    const int qb = p.causal ? nqb - 1 - (int)blockIdx.x : (int)blockIdx.x;  // heaviest first
+    const int per_xcd = (n_groups + kXcds - 1) / kXcds;
+    const int logical = (blockIdx.x % kXcds) * per_xcd + blockIdx.x / kXcds;
+    if (logical >= n_groups) return;
+    const int pair = logical / nqb, rank = logical % nqb;
+    const int qb = p.causal ? nqb - 1 - rank : rank;
     const int groups_per_kv = p.G / HPW;
-    const int g = blockIdx.y / groups_per_kv;
-    const int h = g * p.G + (blockIdx.y % groups_per_kv) * HPW + wave % HPW;
-    const int b = blockIdx.z;
-    const int q0 = qb * BM;                     // first row of the workgroup
-    const int qw0 = q0 + (wave / HPW) * 32;     // first row of this wave
-    const int off = p.Sk - p.Sq;                // bottom-right causal alignment
+    const int b = pair / (p.Hkv * groups_per_kv);
+    const int gy = pair % (p.Hkv * groups_per_kv);
+    const int g = gy / groups_per_kv;
+    const int h = g * p.G + (gy % groups_per_kv) * HPW + wave % HPW;
+    const int q0 = qb * BM;
+    const int qw0 = q0 + (wave / HPW) * 32 * QC;  // first row of this wave
+    const int off = p.Sk - p.Sq;             // bottom-right causal alignment
 
     const uint16_t* qg = (const uint16_t*)p.q + ((size_t)b * p.Hq + h) * p.Sq * R;
     const uint16_t* kg = (const uint16_t*)p.k + ((size_t)b * p.Hkv + g) * p.Sk * R;
     const uint16_t* vg = (const uint16_t*)p.v + ((size_t)b * p.Hkv + g) * p.Sk * DV;
     uint16_t* og = (uint16_t*)p.o + ((size_t)b * p.Hq + h) * p.Sq * DV;
-
-    // Q^T operand: query row qw0 + col, dims 16m + 8 half .. +7
-    const int qrow = qw0 + col;
-    bf16x8 qreg[KSTEPS];
-#pragma unroll
-    for (int m = 0; m < KSTEPS; ++m) {
-        uint4 w = qrow < p.Sq ? *(const uint4*)(qg + (size_t)qrow * R + 16 * m + 8 * half) : make_uint4(0, 0, 0, 0);
-        qreg[m] = __builtin_bit_cast(bf16x8, w);
-    }
 
     int key_end = p.Sk;
     if (p.causal) {
@@ -164,128 +212,216 @@ __global__ __launch_bounds__(kThreads, 2) void prefill_bf16_kernel(const Prefill
         key_end = last < key_end ? last : key_end;
     }
     const int ntiles = (key_end + kBN - 1) / kBN;
-    // last key any row of this wave may see
-    const int wave_last_key = p.causal ? qw0 + 31 + off : p.Sk - 1;
+    const TileLanes<R, DV, NT> tl(tid);
+    load_tile<R, DV, NT>(tl, sm.k[0], sm.v[0], kg, vg, 0, p.Sk, tid);
 
-    f32x16 o[DBLK];
+    // Q^T operands: column block qc holds query rows qw0 + 32 qc + col, dims 16m + 8 half .. +7
+    bf16x8 qreg[QC][KSTEPS];
 #pragma unroll
-    for (int d = 0; d < DBLK; ++d)
+    for (int qc = 0; qc < QC; ++qc) {
+        const int qrow = qw0 + 32 * qc + col;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) o[d][v] = 0.f;
-    float m_ref = -INFINITY;  // running reference maximum (log2 domain) of this lane's row
-    float lsum = 0.f;         // this lane's half of the row sum
+        for (int m = 0; m < KSTEPS; ++m) {
+            const uint4 w =
+                qrow < p.Sq ? *(const uint4*)(qg + (size_t)qrow * R + 16 * m + 8 * half) : make_uint4(0, 0, 0, 0);
+            qreg[qc][m] = __builtin_bit_cast(bf16x8, w);
+        }
+    }
+    const int wave_last_key = p.causal ? qw0 + 32 * QC - 1 + off : p.Sk - 1;  // last key any row of the wave sees
+
+    f32x16 o[QC][DBLK];
+#pragma unroll
+    for (int qc = 0; qc < QC; ++qc)
+#pragma unroll
+        for (int d = 0; d < DBLK; ++d)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) o[qc][d][v] = 0.f;
+    float m_ref[QC], lsum[QC];  // running reference maxima (log2 domain); this lane's half of each row sum
+#pragma unroll
+    for (int qc = 0; qc < QC; ++qc) {
+        m_ref[qc] = -INFINITY;
+        lsum[qc] = 0.f;
+    }
     const float c = p.qscale;
 
-    TileRegs<R, DV> regs;
-    load_tile<R, DV>(regs, kg, vg, 0, p.Sk, tid);
-    store_tile<R, DV>(regs, sm.k[0], sm.vt[0], tid);
+    // Lane byte offsets of the LDS operands. The row swizzles reduce to lane
+    // constants here: for K rows kb*32 + col the swizzle term depends on col
+    // only, for the V rows read below on lane % 16 only.
+    uint32_t kaddr[KSTEPS];
+#pragma unroll
+    for (int m = 0; m < KSTEPS; ++m) kaddr[m] = (uint32_t)((col * R + (((2 * m + half) ^ swz<R, false>(col)) * 8)) * 2);
+    uint32_t vaddr[DBLK];
+    {
+        const int li = lane & 15, grp = lane >> 4;
+        const int sv = swz<DV, true>(li >> 2);
+#pragma unroll
+        for (int d = 0; d < DBLK; ++d) {
+            const int col0 = 32 * d + 16 * (grp & 1) + 4 * (li & 3);
+            const int r1 = 4 * half + (li >> 2);
+            vaddr[d] = (uint32_t)((r1 * DV + (((col0 >> 3) ^ sv) * 8) + (col0 & 7)) * 2);
+        }
+    }
+    wait_loads();
     __syncthreads();
 
     for (int t = 0; t < ntiles; ++t) {
         const int cur = t & 1;
         const int base = t * kBN;
-        if (t + 1 < ntiles) load_tile<R, DV>(regs, kg, vg, base + kBN, p.Sk, tid);
+        if (t + 1 < ntiles) load_tile<R, DV, NT>(tl, sm.k[cur ^ 1], sm.v[cur ^ 1], kg, vg, base + kBN, p.Sk, tid);
 
         if (base <= wave_last_key) {
             const uint16_t* ks = sm.k[cur];
-            const uint16_t* vts = sm.vt[cur];
-            // ---- S^T = K Q^T for the two 32-key blocks
-            f32x16 s[2];
+            const uint16_t* vs = sm.v[cur];
+            // ---- S^T = K Q^T: two 32-key blocks x two query blocks
+            f32x16 s[QC][2];
+#pragma unroll
+            for (int qc = 0; qc < QC; ++qc)
+#pragma unroll
+                for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) s[qc][kb][v] = 0.f;
 #pragma unroll
             for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-                for (int v = 0; v < 16; ++v) s[kb][v] = 0.f;
-#pragma unroll
                 for (int m = 0; m < KSTEPS; ++m) {
-                    const bf16x8 a = *(const bf16x8*)(ks + (kb * 32 + col) * KS + 16 * m + 8 * half);
-                    s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[m], s[kb], 0, 0, 0);
+                    const bf16x8 a = *(const bf16x8*)((const char*)ks + kaddr[m] + kb * 32 * R * 2);
+#pragma unroll
+                    for (int qc = 0; qc < QC; ++qc)
+                        s[qc][kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[qc][m], s[qc][kb], 0, 0, 0);
                 }
             }
             // ---- causal / ragged-tail mask, only where the tile crosses it
             const bool needs_mask = (p.causal && base + kBN - 1 > qw0 + off) || base + kBN > p.Sk;
             if (needs_mask) {
-                const int limit = p.causal ? qrow + off : p.Sk - 1;
-                const int lim = limit < p.Sk - 1 ? limit : p.Sk - 1;
 #pragma unroll
-                for (int kb = 0; kb < 2; ++kb)
+                for (int qc = 0; qc < QC; ++qc) {
+                    const int qrow = qw0 + 32 * qc + col;
+                    int lim = p.causal ? qrow + off : p.Sk - 1;
+                    lim = lim < p.Sk - 1 ? lim : p.Sk - 1;
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) {
-                        const int key = base + kb * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-                        if (key > lim) s[kb][v] = -INFINITY;
-                    }
+                    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) {
+                            const int key = base + kb * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
+                            if (key > lim) s[qc][kb][v] = -INFINITY;
+                        }
+                }
             }
-            // ---- row maximum (in-lane over 32 keys, then across the halves)
-            float mx = s[0][0];
+            // ---- row maxima and lazy rescale for each query block (the only branches)
 #pragma unroll
-            for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[0][v]);
+            for (int qc = 0; qc < QC; ++qc) {
+                float mx = s[qc][0][0];
 #pragma unroll
-            for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[1][v]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float mx2 = mx * c;
-            // each row moves its own reference only; the branch is taken by the
-            // whole wave when any row needs it
-            const bool need = mx2 > m_ref + 8.f;
-            if (__any(need)) {
-                const float alpha = need ? exp2_fast(m_ref - mx2) : 1.f;
-                m_ref = need ? mx2 : m_ref;
-                lsum *= alpha;
+                for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[qc][0][v]);
 #pragma unroll
-                for (int d = 0; d < DBLK; ++d)
+                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[qc][1][v]);
+                mx = xor32_max(mx);
+                const float mx2 = mx * c;
+                // each row moves its own reference; the branch is taken by the whole
+                // wave when any row needs it
+                const bool need = mx2 > m_ref[qc] + 8.f;
+                if (__any(need)) {
+                    const float alpha = need ? exp2_fast(m_ref[qc] - mx2) : 1.f;
+                    m_ref[qc] = need ? mx2 : m_ref[qc];
+                    lsum[qc] *= alpha;
 #pragma unroll
-                    for (int v = 0; v < 16; ++v) o[d][v] *= alpha;
+                    for (int d = 0; d < DBLK; ++d)
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) o[qc][d][v] *= alpha;
+                }
             }
-            // ---- probabilities -> bf16 B operands of O^T = V^T P^T
-            bf16x8 pb[4];
+            // ---- probabilities and O^T += V^T P^T, k-step by k-step. Each V^T operand
+            // is read once for both query blocks, one k-step ahead; within a k-step
+            // the matrix operations of query block 0 are interleaved with the
+            // vector work producing block 1's probabilities, and those of block 1
+            // with block 0's next probabilities, so one wave keeps both pipes busy
+            bf16x8 va[DBLK];
+#pragma unroll
+            for (int d = 0; d < DBLK; ++d) va[d] = vt_operand<DV>(vs, vaddr[d], 0);
+            bf16x8 p0 = prob_step(s[0], 0, m_ref[0], c, lsum[0]);
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                uint32_t w[4];
+                __builtin_amdgcn_sched_barrier(0);
+                bf16x8 vb[DBLK];
+                if (q < 3) {
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float p0 = exp2_fast(fmaf(s[q >> 1][8 * (q & 1) + 2 * i], c, -m_ref));
-                    const float p1 = exp2_fast(fmaf(s[q >> 1][8 * (q & 1) + 2 * i + 1], c, -m_ref));
-                    w[i] = pack_bf16(p0, p1);
-                    lsum = add_bf16_pair(w[i], lsum);
+                    for (int d = 0; d < DBLK; ++d) vb[d] = vt_operand<DV>(vs, vaddr[d], q + 1);
                 }
-                pb[q] = __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+                bf16x8 p1 = p0;
+                if constexpr (QC == 2) p1 = prob_step(s[QC - 1], q, m_ref[QC - 1], c, lsum[QC - 1]);
+                bf16x8 p0n = p0;
+                if (q < 3) p0n = prob_step(s[0], q + 1, m_ref[0], c, lsum[0]);
+#pragma unroll
+                for (int d = 0; d < DBLK; ++d)
+                    o[0][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[d], p0, o[0][d], 0, 0, 0);
+                if constexpr (QC == 2) {
+#pragma unroll
+                    for (int d = 0; d < DBLK; ++d)
+                        o[QC - 1][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[d], p1, o[QC - 1][d], 0, 0, 0);
+                }
+                // schedule: operand reads first, then one MFMA per few vector ops
+                __builtin_amdgcn_sched_group_barrier(0x100, 4 * DBLK, 0);
+#pragma unroll
+                for (int i = 0; i < QC * DBLK; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x402, 6, 0);
+                }
+                if (q < 3) {
+                    p0 = p0n;
+#pragma unroll
+                    for (int d = 0; d < DBLK; ++d) va[d] = vb[d];
+                }
             }
-            // ---- O^T += V^T P^T
-#pragma unroll
-            for (int q = 0; q < 4; ++q)
-#pragma unroll
-                for (int d = 0; d < DBLK; ++d) {
-                    const bf16x8 a = *(const bf16x8*)(vts + (d * 32 + col) * kVtStride + 16 * q + 8 * half);
-                    o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pb[q], o[d], 0, 0, 0);
-                }
         }
 
-        if (t + 1 < ntiles) store_tile<R, DV>(regs, sm.k[cur ^ 1], sm.vt[cur ^ 1], tid);
+        if (t + 1 < ntiles) wait_loads();  // this wave's part of the next tile has landed
         __syncthreads();
     }
 
     // ---- epilogue: normalise and store bf16 rows
-    const float ltot = lsum + __shfl_xor(lsum, 32);
-    const float inv = 1.f / ltot;
-    if (qrow < p.Sq) {
-        uint16_t* orow = og + (size_t)qrow * DV;
 #pragma unroll
-        for (int d = 0; d < DBLK; ++d)
+    for (int qc = 0; qc < QC; ++qc) {
+        const float ltot = xor32_sum(lsum[qc]);
+        const float inv = 1.f / ltot;
+        const int qrow = qw0 + 32 * qc + col;
+        if (qrow < p.Sq) {
+            uint16_t* orow = og + (size_t)qrow * DV;
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                uint2 w;
-                w.x = pack_bf16(o[d][4 * j] * inv, o[d][4 * j + 1] * inv);
-                w.y = pack_bf16(o[d][4 * j + 2] * inv, o[d][4 * j + 3] * inv);
-                *(uint2*)(orow + d * 32 + 8 * j + 4 * half) = w;
-            }
+            for (int d = 0; d < DBLK; ++d)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    uint2 w;
+                    w.x = pack_bf16(o[qc][d][4 * j] * inv, o[qc][d][4 * j + 1] * inv);
+                    w.y = pack_bf16(o[qc][d][4 * j + 2] * inv, o[qc][d][4 * j + 3] * inv);
+                    *(uint2*)(orow + d * 32 + 8 * j + 4 * half) = w;
+                }
+        }
     }
 }
 
-template <int R, int DV>
+template <int R, int DV, int QC, int NW>
 static hipError_t run(const PrefillParams& p, hipStream_t st) {
     const int HPW = gcd4(p.G);
-    const int BM = 32 * (4 / HPW);
-    dim3 grid((p.Sq + BM - 1) / BM, p.Hkv * (p.G / HPW), p.B);
-    hipLaunchKernelGGL((prefill_bf16_kernel<R, DV>), grid, dim3(kThreads), 0, st, p);
+    const int BM = 32 * QC * (NW / HPW);
+    const long nqb = (p.Sq + BM - 1) / BM;
+    const long groups = nqb * p.Hkv * (p.G / HPW) * p.B;
+    const long launched = (groups + kXcds - 1) / kXcds * kXcds;
+    if (launched > 0x7fffffffL) return hipErrorInvalidValue;
+    hipLaunchKernelGGL((prefill_bf16_kernel<R, DV, QC, NW>), dim3((unsigned)launched), dim3(64 * NW), 0, st, p,
+                       (int)groups);
     return hipGetLastError();
+}
+
+#ifndef TK_PREFILL_QC
+#define TK_PREFILL_QC 1
+#endif
+#ifndef TK_PREFILL_WAVES
+#define TK_PREFILL_WAVES 4
+#endif
+
+template <int R, int DV>
+static hipError_t run(const PrefillParams& p, hipStream_t st) {
+    return run<R, DV, TK_PREFILL_QC, TK_PREFILL_WAVES>(p, st);
 }
 
 template <int R>
