@@ -47,6 +47,9 @@ def parse():
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget for the oracle's host timing")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only copy MIB MiB device to device three times (reads and writes a known number "
+                         "of bytes, to scale the FETCH_SIZE / WRITE_SIZE counters) and exit")
     return ap.parse_args()
 
 
@@ -175,11 +178,25 @@ def cpu_baseline(spec, budget_s: float):
                                         f"{el:.1f} s", "seconds_per_step": round(el / reps, 4)}
 
 
+def copy_calibration(mib: int, dev):
+    """A plain streaming kernel of known size: each launch reads ``mib`` MiB once and
+    writes ``mib`` MiB once (an elementwise bitwise-not, so it is a shader kernel and
+    not a DMA-engine copy)."""
+    import torch
+    n = mib << 20
+    src = torch.ones(n // 4, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.bitwise_not(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n, "launches": 3}))
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py: this build measures one GPU only; the thin-key attention path is not sharded "
-              "across GPUs (see DESIGN.md for how it would shard). Run with --gpus 1.", file=sys.stderr)
+        print("bench.py: measures one GPU only; the thin-key attention kernels are not sharded across "
+              "GPUs. Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
     import torch
     from synth import WORKLOADS
@@ -188,6 +205,9 @@ def main():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
     dev = torch.device("cuda", 0)
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration, dev)
+        return
     main_name = args.only or "mistral_decode_b16"
     results = {}
     order = [main_name] if (args.no_secondary or args.only) else \
