@@ -16,7 +16,11 @@ The JSON line reports, besides the contract fields:
                 same workload (not an optimisation target);
   secondary     the other workloads, each with its own roofline: causal prefill
                 at 8192 tokens (bf16 MFMA), the 131072-token paged decode, the
-                fp8-key decode, and the GPT-2 fp32 prefill.
+                fp8-key decode, and the GPT-2 fp32 prefill;
+  fullkey_control  the batch-16 decode, the 8192-token prefill and the
+                131072-token paged decode again with standard-width keys (r = 128,
+                same values), and the thin-key speedup over them next to the
+                byte (decode) or FLOP (prefill) ratio that bounds it.
 """
 from __future__ import annotations
 
@@ -46,6 +50,7 @@ def parse():
     ap.add_argument("--only", default=None, help="time just this workload (e.g. for profiling)")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-fullkey", action="store_true", help="skip the full-key (r = 128) control timings")
     ap.add_argument("--cpu-seconds", type=float, default=10.0, help="budget for the oracle's host timing")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only copy MIB MiB device to device three times (reads and writes a known number "
@@ -199,7 +204,7 @@ def main():
               "GPUs. Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
     import torch
-    from synth import WORKLOADS
+    from synth import FULLKEY, WORKLOADS
 
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
@@ -213,20 +218,38 @@ def main():
     order = [main_name] if (args.no_secondary or args.only) else \
         [main_name] + [n for n in ("mistral_prefill_s8192", "longctx_paged_decode", "fp8key_decode",
                                    "gpt2_prefill_f32") if n != main_name]
-    for name in order:
-        spec = WORKLOADS[name]
+    def run(name, spec, main=False):
         print(f"bench: timing {name}", file=sys.stderr, flush=True)
         if hasattr(spec, "ctx"):
             big = spec.batch * spec.h_kv * spec.ctx * (spec.r + spec.d_v) * 2 > (1 << 30)
             calls = decode_setup(spec, dev, 1 if big else args.rotate)
-            steps = args.steps if name == main_name else max(10, args.steps // 10)
-            results[name] = decode_result(name, spec, calls, steps, args.warmup)
-            results[name]["rotate"] = len(calls)
+            steps = args.steps if main else max(10, args.steps // 10)
+            res = decode_result(name, spec, calls, steps, args.warmup)
+            res["rotate"] = len(calls)
             del calls
             torch.cuda.empty_cache()
         else:
-            steps = args.steps if name == main_name else max(5, args.steps // 20)
-            results[name] = prefill_result(name, spec, dev, steps, min(args.warmup, 3))
+            steps = args.steps if main else max(5, args.steps // 20)
+            res = prefill_result(name, spec, dev, steps, min(args.warmup, 3))
+        return res
+
+    for name in order:
+        results[name] = run(name, WORKLOADS[name], main=name == main_name)
+    fullkey = []
+    if not (args.no_fullkey or args.only or args.no_secondary):
+        from paper_2603_04427_amd import accounting as acc
+        for name, spec in FULLKEY.items():
+            thin = results[name[:-len("_fullkey")]]
+            full = run(name, spec)
+            tspec = WORKLOADS[name[:-len("_fullkey")]]
+            if hasattr(spec, "ctx"):
+                ideal = acc.decode_bytes(spec.lens, spec.h_q, spec.h_kv, spec.r, spec.d_v) / \
+                    acc.decode_bytes(tspec.lens, tspec.h_q, tspec.h_kv, tspec.r, tspec.d_v)
+            else:
+                ideal = (spec.r + spec.d_v) / (tspec.r + tspec.d_v)
+            full["thin_key_speedup"] = round(full["roofline"]["kernel_ms"] / thin["roofline"]["kernel_ms"], 3)
+            full["ideal_speedup"] = round(ideal, 3)
+            fullkey.append(full)
     m = results[main_name]
     spec = WORKLOADS[main_name]
     is_decode = hasattr(spec, "ctx")
@@ -247,6 +270,8 @@ def main():
         print("bench: oracle on the host cores", file=sys.stderr, flush=True)
         line["cpu_baseline"] = cpu_baseline(spec, args.cpu_seconds)
     line["secondary"] = [results[n] for n in order if n != main_name]
+    if fullkey:
+        line["fullkey_control"] = fullkey
     line["device"] = torch.cuda.get_device_name(0)
     print(json.dumps(line), flush=True)
 

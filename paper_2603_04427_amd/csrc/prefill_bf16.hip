@@ -6,11 +6,10 @@
 // cores (v_mfma_f32_32x32x16_bf16); the softmax runs on the vector ALUs.
 //
 // Work decomposition
-//  * A workgroup is 4 waves. Each wave owns 64 query rows (two 32-column MFMA
-//    blocks) of one query head; the workgroup covers HPW = gcd(G, 4) heads of
-//    one KV group and 4 / HPW row blocks, so each K/V tile in LDS serves every
-//    wave, and each LDS operand read feeds two MFMAs (LDS bandwidth, about
-//    128 bytes per clock per CU, would otherwise bound the kernel).
+//  * A workgroup is 4 waves. Each wave owns 32 query rows (one 32-column MFMA
+//    block; QC = 2 gives it 64 rows, each LDS operand read then feeding two
+//    MFMAs) of one query head; the workgroup covers HPW = gcd(G, 4) heads of one
+//    KV group and 4 / HPW row blocks, so each K/V tile in LDS serves every wave.
 //  * 64-key tiles are double-buffered in LDS and filled straight from global
 //    memory (global_load_lds, 16 bytes per lane), K and V both in their memory
 //    layout with the 16-byte chunks of each row XOR-swizzled so that the
@@ -95,29 +94,44 @@ struct TileLanes {
     }
 };
 
-// Issue the copies of the tile starting at key `base`. Rows at or past Sk (only
-// in a ragged last tile) re-read row Sk - 1: finite values, masked later.
+// Issue the copies of the tile starting at key `base` (wave `wave` copies its
+// 1 KB slices). A full tile needs no vector arithmetic: the global base and the
+// LDS destination are wave-uniform and the lane offsets are precomputed. Rows
+// at or past Sk (only in a ragged last tile) re-read row Sk - 1: finite values,
+// masked later.
 template <int R, int DV, int NT>
 __device__ __forceinline__ void load_tile(const TileLanes<R, DV, NT>& tl, uint16_t* ks, uint16_t* vs,
-                                          const uint16_t* kg, const uint16_t* vg, int base, int Sk, int tid) {
+                                          const uint16_t* kg, const uint16_t* vg, int base, int Sk, int wave) {
     using T = TileLanes<R, DV, NT>;
-    const int wave_base = tid & ~63;
-    const bool full = base + kBN <= Sk;  // workgroup-uniform
+    const int wave_base = wave * 64;
     const char* kt = (const char*)(kg + (size_t)base * R);
     const char* vt = (const char*)(vg + (size_t)base * DV);
+    if (base + kBN <= Sk) {  // workgroup-uniform
+#pragma unroll
+        for (int i = 0; i < T::KL; ++i) {
+            if (T::KC % NT != 0 && wave_base + i * NT >= T::KC) break;
+            __builtin_amdgcn_global_load_lds((const void*)(kt + tl.k_off[i]), (lds_ptr)(ks + (wave_base + i * NT) * 8),
+                                             16, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < T::VL; ++i) {
+            if (T::VC % NT != 0 && wave_base + i * NT >= T::VC) break;
+            __builtin_amdgcn_global_load_lds((const void*)(vt + tl.v_off[i]), (lds_ptr)(vs + (wave_base + i * NT) * 8),
+                                             16, 0, 0);
+        }
+        return;
+    }
     const int last = Sk - base - 1;
 #pragma unroll
     for (int i = 0; i < T::KL; ++i) {
         if (T::KC % NT != 0 && wave_base + i * NT >= T::KC) break;
-        uint32_t off = tl.k_off[i];
-        if (!full && (int)tl.k_row[i] > last) off -= (tl.k_row[i] - last) * R * 2;
+        const uint32_t off = (int)tl.k_row[i] > last ? tl.k_off[i] - (tl.k_row[i] - last) * R * 2 : tl.k_off[i];
         __builtin_amdgcn_global_load_lds((const void*)(kt + off), (lds_ptr)(ks + (wave_base + i * NT) * 8), 16, 0, 0);
     }
 #pragma unroll
     for (int i = 0; i < T::VL; ++i) {
         if (T::VC % NT != 0 && wave_base + i * NT >= T::VC) break;
-        uint32_t off = tl.v_off[i];
-        if (!full && (int)tl.v_row[i] > last) off -= (tl.v_row[i] - last) * DV * 2;
+        const uint32_t off = (int)tl.v_row[i] > last ? tl.v_off[i] - (tl.v_row[i] - last) * DV * 2 : tl.v_off[i];
         __builtin_amdgcn_global_load_lds((const void*)(vt + off), (lds_ptr)(vs + (wave_base + i * NT) * 8), 16, 0, 0);
     }
 }
@@ -213,7 +227,7 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_ke
     }
     const int ntiles = (key_end + kBN - 1) / kBN;
     const TileLanes<R, DV, NT> tl(tid);
-    load_tile<R, DV, NT>(tl, sm.k[0], sm.v[0], kg, vg, 0, p.Sk, tid);
+    load_tile<R, DV, NT>(tl, sm.k[0], sm.v[0], kg, vg, 0, p.Sk, wave);
 
     // Q^T operands: column block qc holds query rows qw0 + 32 qc + col, dims 16m + 8 half .. +7
     bf16x8 qreg[QC][KSTEPS];
@@ -267,7 +281,7 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_ke
     for (int t = 0; t < ntiles; ++t) {
         const int cur = t & 1;
         const int base = t * kBN;
-        if (t + 1 < ntiles) load_tile<R, DV, NT>(tl, sm.k[cur ^ 1], sm.v[cur ^ 1], kg, vg, base + kBN, p.Sk, tid);
+        if (t + 1 < ntiles) load_tile<R, DV, NT>(tl, sm.k[cur ^ 1], sm.v[cur ^ 1], kg, vg, base + kBN, p.Sk, wave);
 
         if (base <= wave_last_key) {
             const uint16_t* ks = sm.k[cur];

@@ -100,6 +100,16 @@ WORKLOADS = {
 }
 
 
+# Full-key controls: the same workloads with standard-width keys (r = d_head =
+# 128, scale 1/sqrt(128)) and the same value streams, so that thin-key and
+# full-key attention can be timed side by side (the decode saving the paper
+# predicts from the byte ratio, Eq. 8-10, and the prefill selection cost).
+FULLKEY = {
+    name + "_fullkey": replace(WORKLOADS[name], name=name + "_fullkey", r=128)
+    for name in ("mistral_decode_b16", "mistral_prefill_s8192", "longctx_paged_decode")
+}
+
+
 def _draw(spec_id: int, tensor: int, shape, device, amp: float = 1.0) -> torch.Tensor:
     n = 1
     for s in shape:

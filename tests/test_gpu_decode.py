@@ -7,7 +7,7 @@ import pytest
 import torch
 
 from gpu_cases import decode_on_gpu, decode_oracle, device, gate, say
-from synth import WORKLOADS, DecodeSpec, make_decode, with_shape
+from synth import FULLKEY, WORKLOADS, DecodeSpec, make_decode, with_shape
 
 pytestmark = pytest.mark.gpu
 
@@ -62,20 +62,24 @@ def test_paged_block_sizes(bs):
     gate(out, ref, "bf16", f"bs={bs}")
 
 
-def test_mistral_decode_b16_full():
-    """Batch 16, 32/8 heads, context 4096, r 32, d_v 128: every output."""
-    spec = WORKLOADS["mistral_decode_b16"]
+@pytest.mark.parametrize("name", ["mistral_decode_b16", "mistral_decode_b16_fullkey"])
+def test_mistral_decode_b16_full(name):
+    """Batch 16, 32/8 heads, context 4096, d_v 128, thin keys (r 32) and the full-key
+    control (r 128): every output."""
+    spec = {**WORKLOADS, **FULLKEY}[name]
     for structured in (False, True):
         out, ref = run_case(spec, structured)
-        mx, rel = gate(out, ref, "bf16", f"mistral_decode_b16 structured={structured}")
+        mx, rel = gate(out, ref, "bf16", f"{name} structured={structured}")
         say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
 
 
-def test_longctx_paged_decode_full_sampled():
-    """Context 131072 in 256-token pages with a permuted table; oracle on 2 of 8 sequences."""
-    spec = WORKLOADS["longctx_paged_decode"]
+@pytest.mark.parametrize("name", ["longctx_paged_decode", "longctx_paged_decode_fullkey"])
+def test_longctx_paged_decode_full_sampled(name):
+    """Context 131072 in 256-token pages with a permuted table, thin keys (r 32) and the
+    full-key control (r 128); oracle on 2 of 8 sequences."""
+    spec = {**WORKLOADS, **FULLKEY}[name]
     out, ref = run_case(spec, structured=True, batches=[0, 7], on_gpu_inputs=True)
-    mx, rel = gate(out, ref, "bf16", "longctx_paged_decode")
+    mx, rel = gate(out, ref, "bf16", name)
     say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
 
 

@@ -6,7 +6,7 @@ import pytest
 import torch
 
 from gpu_cases import device, gate, prefill_on_gpu, prefill_oracle, prefill_rows_oracle, say
-from synth import WORKLOADS, PrefillSpec, make_prefill, with_shape
+from synth import FULLKEY, WORKLOADS, PrefillSpec, make_prefill, with_shape
 
 pytestmark = pytest.mark.gpu
 
@@ -68,11 +68,13 @@ ROWS = [0, 1, 7, 8, 31, 32, 63, 64, 65, 127, 128, 1000, 4095, 4096, 8190, 8191]
 
 
 @pytest.mark.parametrize("structured", [False, True])
-def test_mistral_prefill_s8192_full_sampled(structured):
-    """Batch 4, 32/8 heads, 8192 tokens, r 32, d_v 128, bf16: the whole call on the GPU,
-    16 rows of 2 sequences (all heads) against the oracle."""
+@pytest.mark.parametrize("name", ["mistral_prefill_s8192", "mistral_prefill_s8192_fullkey"])
+def test_mistral_prefill_s8192_full_sampled(name, structured):
+    """Batch 4, 32/8 heads, 8192 tokens, d_v 128, bf16, thin keys (r 32) and the
+    full-key control (r 128): the whole call on the GPU, 16 rows of 2 sequences (all
+    heads) against the oracle."""
     dev = device()
-    spec = WORKLOADS["mistral_prefill_s8192"]
+    spec = {**WORKLOADS, **FULLKEY}[name]
     p = make_prefill(spec, device=dev, structured=structured)
     say(f"prefill full {spec.name} structured={structured}")
     out = prefill_on_gpu(p, spec, dev)
