@@ -17,6 +17,10 @@ The JSON line reports, besides the contract fields:
   secondary     the other workloads, each with its own roofline: causal prefill
                 at 8192 tokens (bf16 MFMA), the 131072-token paged decode, the
                 fp8-key decode, and the GPT-2 fp32 prefill;
+  cache_append  the cache write before decode (tk_cache_append): 8192 new tokens
+                per (sequence, KV head) of the prefill shape with bf16 and with
+                fp8 keys (quantised on write), and one decode token of the
+                batch-16 shape;
   fullkey_control  the batch-16 decode, the 8192-token prefill and the
                 131072-token paged decode again with standard-width keys (r = 128,
                 same values), and the thin-key speedup over them next to the
@@ -158,6 +162,34 @@ def prefill_result(name, spec, dev, steps, warmup):
     }
 
 
+def append_result(name, B, Hkv, T, r, dv, fp8, dev, steps, warmup):
+    """tk_cache_append of T new tokens per (sequence, KV head) into a contiguous cache."""
+    import torch
+    from paper_2603_04427_amd import prepare_cache_append
+    from synth import normal, stream_key
+
+    kn = normal(stream_key(20, 0), B * Hkv * T * r, device=dev).view(B, Hkv, T, r).to(torch.bfloat16)
+    vn = normal(stream_key(20, 1), B * Hkv * T * dv, device=dev).view(B, Hkv, T, dv).to(torch.bfloat16)
+    kc = torch.zeros(B, Hkv, T, r, dtype=torch.uint8 if fp8 else torch.bfloat16, device=dev)
+    vc = torch.zeros(B, Hkv, T, dv, dtype=torch.bfloat16, device=dev)
+    ks = torch.zeros(B, Hkv, T, dtype=torch.float32, device=dev) if fp8 else None
+    pos = torch.zeros(B, dtype=torch.int32, device=dev)
+    call = prepare_cache_append(kn, vn, pos, kc, vc, k_scale=ks)
+    wall, ev = time_calls([call], steps, warmup)
+    tokens = B * Hkv * T
+    nbytes = tokens * (r * 2 + dv * 2) + B * 4 + tokens * ((r + 4) if fp8 else r * 2) + tokens * dv * 2
+    del kn, vn, kc, vc, ks, call
+    torch.cuda.empty_cache()
+    from paper_2603_04427_amd import accounting as acc
+    return {
+        "workload": name, "value": round(nbytes / wall / 1e9, 1), "unit": "GB/s",
+        "ms_per_call": round(wall * 1e3, 5),
+        "roofline": {"bound": "hbm", "achieved": round(nbytes / ev / 1e9, 1), "peak": acc.HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(nbytes / ev / 1e9 / acc.HBM_PEAK_GBS, 4),
+                     "traffic": None, "algorithmic_bytes": nbytes, "kernel_ms": round(ev * 1e3, 5)},
+    }
+
+
 def cpu_baseline(spec, budget_s: float):
     """The fp64 oracle on the host cores over whole decode steps of the workload,
     repeated until the time budget is used (at least once)."""
@@ -250,6 +282,13 @@ def main():
             full["thin_key_speedup"] = round(full["roofline"]["kernel_ms"] / thin["roofline"]["kernel_ms"], 3)
             full["ideal_speedup"] = round(ideal, 3)
             fullkey.append(full)
+    appends = []
+    if not (args.only or args.no_secondary):
+        for name, B, T, fp8 in (("cache_append_s8192", 4, 8192, False), ("cache_append_fp8_s8192", 4, 8192, True),
+                                ("cache_append_decode_b16", 16, 1, False)):
+            print(f"bench: timing {name}", file=sys.stderr, flush=True)
+            appends.append(append_result(name, B, 8, T, 32, 128, fp8, dev, max(10, args.steps // 10),
+                                         args.warmup))
     m = results[main_name]
     spec = WORKLOADS[main_name]
     is_decode = hasattr(spec, "ctx")
@@ -272,6 +311,8 @@ def main():
     line["secondary"] = [results[n] for n in order if n != main_name]
     if fullkey:
         line["fullkey_control"] = fullkey
+    if appends:
+        line["cache_append"] = appends
     line["device"] = torch.cuda.get_device_name(0)
     print(json.dumps(line), flush=True)
 

@@ -124,6 +124,37 @@ tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache
                          int num_blocks,
                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 
+/*
+ * Append n_new tokens per sequence to a thin-key / full-value cache: the write
+ * that precedes decode (the thin-K / full-V cache of Sec. 2.4, Eq. 9). Token t
+ * of sequence b and KV head g is stored at cache position positions[b] + t.
+ *
+ *   K_new [batch, H_kv, n_new, r] bf16      V_new [batch, H_kv, n_new, d_v] bf16
+ *   positions [batch] int32 (device): first position written for sequence b.
+ *   K_cache, V_cache, k_scale, block_table, block_size, max_blocks_per_seq,
+ *       num_blocks, k_dtype: the cache layouts of tk_attn_decode. A contiguous
+ *       cache holds max_ctx positions per sequence; a paged one
+ *       block_size * max_blocks_per_seq (max_ctx is then not used); block_size
+ *       must be a power of two.
+ *   k_dtype TK_BF16 copies the key rows. TK_FP8_E4M3 quantises each key row on
+ *       the way in (the composition with quantisation of Sec. 6): its scale is
+ *       max|k| / 448 over the row's r entries (1.0 for an all-zero row), stored in
+ *       k_scale, and each entry becomes the OCP E4M3 code of k / scale rounded to
+ *       nearest-even; both steps in fp32 with IEEE division.
+ * A token whose position is negative or not below the capacity, or whose block
+ * table entry lies outside [0, num_blocks), is not written (nothing else is
+ * touched). Tokens of one call must land on distinct positions. V_cache rows and
+ * bf16 key rows are bit-exact copies.
+ * Supported: r in {16, 32, 64, 128}; d_v in {64, 128}; batch * H_kv <= 65535.
+ * batch == 0 or n_new == 0 is a no-op. Pointers to bf16 data and the caches must
+ * be 16-byte aligned.
+ */
+tk_status tk_cache_append(const void* K_new, const void* V_new, int batch, int H_kv, int n_new, int r, int d_v,
+                          const int32_t* positions, void* K_cache, void* V_cache, int max_ctx,
+                          tk_dtype k_dtype, float* k_scale,
+                          const int32_t* block_table, int block_size, int max_blocks_per_seq,
+                          int num_blocks, hipStream_t stream);
+
 /* A static, human-readable name for a status code. Never NULL. */
 const char* tk_status_str(tk_status status);
 

@@ -5,6 +5,6 @@ ABI of include/tk_attn.h); ``binding`` exposes its entry points under the same
 names, plus prepared (pre-marshalled) calls for timing loops. ``accounting``
 holds the byte/FLOP accounting used for roofline figures.
 """
-from .binding import (PreparedCall, TkError, prepare_decode, prepare_prefill,  # noqa: F401
-                      tk_attn_decode, tk_attn_decode_workspace_bytes, tk_attn_prefill, tk_status_str,
-                      tk_version)
+from .binding import (PreparedCall, TkError, prepare_cache_append, prepare_decode, prepare_prefill,  # noqa: F401
+                      tk_attn_decode, tk_attn_decode_workspace_bytes, tk_attn_prefill, tk_cache_append,
+                      tk_status_str, tk_version)

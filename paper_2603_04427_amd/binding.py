@@ -26,6 +26,7 @@ SIGNATURES = {
     "tk_attn_decode_workspace_bytes": ([_i, _i, _i, _i, _i], _sz),
     "tk_attn_decode": ([_vp, _vp, _vp, _vp, _i, _i, _i, _vp, _i, _i, _i, _f, _i, _vp, _vp, _i, _i, _i,
                         _vp, _sz, _vp], _i),
+    "tk_cache_append": ([_vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _i, _vp, _vp, _i, _i, _i, _vp], _i),
     "tk_status_str": ([_i], ctypes.c_char_p),
     "tk_version": ([], _i),
 }
@@ -203,3 +204,55 @@ def tk_attn_decode(Q: torch.Tensor, K_cache: torch.Tensor, V_cache: torch.Tensor
     A workspace passed in must have been zeroed before its first use (see include/tk_attn.h)."""
     return prepare_decode(Q, K_cache, V_cache, ctx_lens, max_ctx, scale, k_scale, block_table, block_size,
                           workspace, O, stream)()
+
+
+def prepare_cache_append(K_new: torch.Tensor, V_new: torch.Tensor, positions: torch.Tensor,
+                         K_cache: torch.Tensor, V_cache: torch.Tensor, k_scale: Optional[torch.Tensor] = None,
+                         block_table: Optional[torch.Tensor] = None, block_size: int = 0,
+                         stream=None) -> PreparedCall:
+    """Append marshalled. K_new [B,Hkv,T,r], V_new [B,Hkv,T,dv] bf16; positions [B] int32; caches as for
+    decode: contiguous [B,Hkv,max_ctx,*] or paged [nblk,Hkv,bs,*] with block_table [B, mb] int32. A uint8 /
+    float8_e4m3fn K_cache (with k_scale fp32) receives E4M3 codes quantised per row."""
+    _check(K_new, "K_new", (torch.bfloat16,), 4)
+    _check(V_new, "V_new", (torch.bfloat16,), 4)
+    _check(positions, "positions", (torch.int32,), 1)
+    _check(K_cache, "K_cache", (torch.bfloat16, torch.uint8, torch.float8_e4m3fn), 4)
+    _check(V_cache, "V_cache", (torch.bfloat16,), 4)
+    B, Hkv, T, r = K_new.shape
+    dv = V_new.shape[3]
+    if tuple(V_new.shape[:3]) != (B, Hkv, T) or positions.shape[0] != B:
+        raise ValueError(f"shape mismatch K_new{tuple(K_new.shape)} V_new{tuple(V_new.shape)} "
+                         f"positions{tuple(positions.shape)}")
+    fp8 = K_cache.dtype != torch.bfloat16
+    if fp8:
+        if k_scale is None:
+            raise ValueError("fp8 keys need k_scale")
+        _check(k_scale, "k_scale", (torch.float32,), 3)
+        K_cache = K_cache.view(torch.uint8)
+    elif k_scale is not None:
+        raise ValueError("k_scale is only for fp8 keys")
+    if K_cache.shape[1] != Hkv or K_cache.shape[3] != r or K_cache.shape[:3] != V_cache.shape[:3] \
+            or V_cache.shape[3] != dv:
+        raise ValueError(f"cache shapes K{tuple(K_cache.shape)} V{tuple(V_cache.shape)} do not match the rows")
+    if k_scale is not None and tuple(k_scale.shape) != tuple(K_cache.shape[:3]):
+        raise ValueError("k_scale must be [*, Hkv, tokens]")
+    if block_table is None:
+        if K_cache.shape[0] != B:
+            raise ValueError("contiguous cache must be [B, Hkv, max_ctx, *]")
+        max_ctx, mb, nblk, block_size = K_cache.shape[2], 0, 0, 0
+    else:
+        _check(block_table, "block_table", (torch.int32,), 2)
+        if block_table.shape[0] != B or block_size != K_cache.shape[2]:
+            raise ValueError("block_table must be [B, mb] and block_size the cache's slot dimension")
+        max_ctx, mb, nblk = 0, block_table.shape[1], K_cache.shape[0]
+    args = (_ptr(K_new), _ptr(V_new), B, Hkv, T, r, dv, _ptr(positions), _ptr(K_cache), _ptr(V_cache),
+            int(max_ctx), TK_FP8_E4M3 if fp8 else TK_BF16, _ptr(k_scale), _ptr(block_table), int(block_size),
+            int(mb), int(nblk), _stream(stream))
+    return PreparedCall("tk_cache_append", args, (K_new, V_new, positions, k_scale, block_table, K_cache))
+
+
+def tk_cache_append(K_new: torch.Tensor, V_new: torch.Tensor, positions: torch.Tensor, K_cache: torch.Tensor,
+                    V_cache: torch.Tensor, k_scale: Optional[torch.Tensor] = None,
+                    block_table: Optional[torch.Tensor] = None, block_size: int = 0, stream=None) -> None:
+    """Write T new tokens per sequence into the cache at positions[b] + t (see include/tk_attn.h)."""
+    prepare_cache_append(K_new, V_new, positions, K_cache, V_cache, k_scale, block_table, block_size, stream)()

@@ -137,4 +137,50 @@ tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache
     return tk::launch_decode(p, r, d_v, hg, fp8, paged, stream);
 }
 
+tk_status tk_cache_append(const void* K_new, const void* V_new, int batch, int H_kv, int n_new, int r, int d_v,
+                          const int32_t* positions, void* K_cache, void* V_cache, int max_ctx, tk_dtype k_dtype,
+                          float* k_scale, const int32_t* block_table, int block_size, int max_blocks_per_seq,
+                          int num_blocks, hipStream_t stream) {
+    if (batch < 0 || H_kv <= 0 || n_new < 0 || r <= 0 || d_v <= 0 || max_ctx < 0) return TK_ERR_INVALID_ARG;
+    if (k_dtype != TK_BF16 && k_dtype != TK_FP8_E4M3) return k_dtype == TK_F32 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
+    const bool fp8 = k_dtype == TK_FP8_E4M3;
+    if (fp8 != (k_scale != nullptr)) return TK_ERR_INVALID_ARG;  // scales iff fp8 keys
+    const bool paged = block_table != nullptr;
+    int bs_log2 = 0;
+    long capacity = max_ctx;
+    if (paged) {
+        if (block_size <= 0 || max_blocks_per_seq <= 0 || num_blocks <= 0) return TK_ERR_INVALID_ARG;
+        bs_log2 = log2_exact(block_size);
+        if (bs_log2 < 0) return TK_ERR_UNSUPPORTED;
+        capacity = (long)block_size * max_blocks_per_seq;
+    } else if (block_size != 0 || max_blocks_per_seq != 0 || num_blocks != 0) {
+        return TK_ERR_INVALID_ARG;  // layout arguments without a table
+    }
+    if (batch == 0 || n_new == 0) return TK_OK;
+    if (!K_new || !V_new || !positions || !K_cache || !V_cache) return TK_ERR_INVALID_ARG;
+    if (!aligned16(K_new) || !aligned16(V_new) || !aligned16(K_cache) || !aligned16(V_cache))
+        return TK_ERR_INVALID_ARG;
+    if (!supported_r(r) || !supported_dv(d_v)) return TK_ERR_UNSUPPORTED;
+    // 32-bit slice indices within one (sequence, KV head); at most 65535 pairs
+    if ((long)n_new * (d_v > r ? d_v : r) / 8 > 0x7fffff00L || (long)batch * H_kv > kMaxGrid)
+        return TK_ERR_UNSUPPORTED;
+
+    tk::AppendParams p{};
+    p.kn = (const uint16_t*)K_new;
+    p.vn = (const uint16_t*)V_new;
+    p.pos = positions;
+    p.kc = (uint8_t*)K_cache;
+    p.ks = k_scale;
+    p.vc = (uint16_t*)V_cache;
+    p.table = block_table;
+    p.B = batch;
+    p.Hkv = H_kv;
+    p.T = n_new;
+    p.capacity = capacity;
+    p.bs_log2 = bs_log2;
+    p.mb = paged ? max_blocks_per_seq : 0;
+    p.num_blocks = paged ? num_blocks : 0;
+    return tk::launch_append(p, r, d_v, fp8, paged, stream);
+}
+
 }  // extern "C"

@@ -42,6 +42,22 @@ DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV);
 tk_status launch_decode(const DecodeParams& p, int R, int DV, int HG, bool fp8, bool paged,
                         hipStream_t stream);
 
+// Cache append: grid-stride over 16-byte row slices of the new tokens.
+struct AppendParams {
+    const uint16_t* kn;         // [B, Hkv, T, R] bf16 new key rows
+    const uint16_t* vn;         // [B, Hkv, T, DV] bf16 new value rows
+    const int32_t* pos;         // [B] first position written
+    uint8_t* kc;                // key cache rows: bf16 (2R bytes) or E4M3 codes (R bytes)
+    float* ks;                  // per key row scale (fp8 only)
+    uint16_t* vc;               // value cache rows
+    const int32_t* table;       // [B, mb] or null
+    int B, Hkv, T;
+    long capacity;              // positions per sequence: max_ctx, or block_size * mb when paged
+    int bs_log2, mb, num_blocks;
+};
+
+tk_status launch_append(const AppendParams& p, int R, int DV, bool fp8, bool paged, hipStream_t stream);
+
 struct PrefillParams {
     const void* q;   // [B, Hq, Sq, R]
     const void* k;   // [B, Hkv, Sk, R]

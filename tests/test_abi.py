@@ -103,3 +103,33 @@ def test_workspace_query_is_pure_and_sized():
     assert ws(16, 30, 8, 4096, 128) == 0 and ws(0, 32, 8, 4096, 128) == 0
     assert ws(8, 32, 8, 131072, 128) >= 8 * 32 * 130 * 4
     assert ws(1, 32, 8, 0, 128) == 256 + 32 * 130 * 4         # empty caches: one split, 32 counters
+
+
+def append(**kw):
+    a = dict(K_new=P, V_new=P, batch=2, H_kv=8, n_new=1, r=32, d_v=128, positions=P, K=P, V=P, max_ctx=4096,
+             k_dtype=tb.TK_BF16, k_scale=None, block_table=None, block_size=0, max_blocks=0, num_blocks=0,
+             stream=None)
+    a.update(kw)
+    return tb.lib().tk_cache_append(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(n_new=-1), tb.TK_ERR_INVALID_ARG),
+    (dict(H_kv=0), tb.TK_ERR_INVALID_ARG),
+    (dict(max_ctx=-1), tb.TK_ERR_INVALID_ARG),
+    (dict(k_dtype=tb.TK_FP8_E4M3), tb.TK_ERR_INVALID_ARG),     # fp8 without scales
+    (dict(k_scale=P), tb.TK_ERR_INVALID_ARG),                  # scales without fp8
+    (dict(k_dtype=tb.TK_F32), tb.TK_ERR_UNSUPPORTED),
+    (dict(block_size=64), tb.TK_ERR_INVALID_ARG),              # layout args without a table
+    (dict(block_table=P, block_size=0, max_blocks=4, num_blocks=8), tb.TK_ERR_INVALID_ARG),
+    (dict(block_table=P, block_size=48, max_blocks=4, num_blocks=8), tb.TK_ERR_UNSUPPORTED),
+    (dict(positions=None), tb.TK_ERR_INVALID_ARG),
+    (dict(V_new=P_ODD), tb.TK_ERR_INVALID_ARG),
+    (dict(r=24), tb.TK_ERR_UNSUPPORTED),
+    (dict(d_v=32), tb.TK_ERR_UNSUPPORTED),
+    (dict(batch=4096, H_kv=32), tb.TK_ERR_UNSUPPORTED),        # more than 65535 (sequence, head) pairs
+    (dict(batch=0), tb.TK_OK),                                 # nothing to do, no launch
+    (dict(n_new=0), tb.TK_OK),
+])
+def test_append_validation(kw, status):
+    assert append(**kw) == status
