@@ -42,7 +42,8 @@ METRIC = "thin-key decode-attn HBM GB/s (% peak); prefill-attn TFLOP/s (% MFMA p
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.json")
 KERNEL_SOURCES = {"decode": "paper_2603_04427_amd/csrc/decode.hip",
                   "prefill_bf16": "paper_2603_04427_amd/csrc/prefill_bf16.hip",
-                  "prefill_f32": "paper_2603_04427_amd/csrc/prefill_f32.hip"}
+                  "prefill_f32": "paper_2603_04427_amd/csrc/prefill_f32.hip",
+                  "append": "paper_2603_04427_amd/csrc/append.hip"}
 
 
 def parse():
@@ -186,7 +187,8 @@ def append_result(name, B, Hkv, T, r, dv, fp8, dev, steps, warmup):
         "ms_per_call": round(wall * 1e3, 5),
         "roofline": {"bound": "hbm", "achieved": round(nbytes / ev / 1e9, 1), "peak": acc.HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(nbytes / ev / 1e9 / acc.HBM_PEAK_GBS, 4),
-                     "traffic": None, "algorithmic_bytes": nbytes, "kernel_ms": round(ev * 1e3, 5)},
+                     "traffic": traffic_for(name, "append"), "algorithmic_bytes": nbytes,
+                     "kernel_ms": round(ev * 1e3, 5)},
     }
 
 
@@ -244,6 +246,17 @@ def main():
     dev = torch.device("cuda", 0)
     if args.copy_calibration:
         copy_calibration(args.copy_calibration, dev)
+        return
+    if args.only and args.only.startswith("cache_append"):
+        cases = {"cache_append_s8192": (4, 8192, False), "cache_append_fp8_s8192": (4, 8192, True),
+                 "cache_append_decode_b16": (16, 1, False)}
+        B, T, fp8 = cases[args.only]
+        res = append_result(args.only, B, 8, T, 32, 128, fp8, dev, args.steps, args.warmup)
+        print(json.dumps({"metric": "cache append HBM GB/s", "value": res["value"], "unit": "GB/s", "n_gpus": 1,
+                          "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_call"],
+                          "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+                          "data": "synthetic", "config": {"workload": args.only}, "roofline": res["roofline"]}),
+              flush=True)
         return
     main_name = args.only or "mistral_decode_b16"
     results = {}
