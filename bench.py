@@ -16,15 +16,16 @@ The JSON line reports, besides the contract fields:
                 same workload (not an optimisation target);
   secondary     the other workloads, each with its own roofline: causal prefill
                 at 8192 tokens (bf16 MFMA), the 131072-token paged decode, the
-                fp8-key decode, and the GPT-2 fp32 prefill;
+                fp8-key and 4-bit-key decodes, and the GPT-2 fp32 prefill;
   cache_append  the cache write before decode (tk_cache_append): 8192 new tokens
-                per (sequence, KV head) of the prefill shape with bf16 and with
-                fp8 keys (quantised on write), and one decode token of the
+                per (sequence, KV head) of the prefill shape with bf16, fp8 and
+                4-bit keys (quantised on write), and one decode token of the
                 batch-16 shape;
-  fullkey_control  the batch-16 decode, the 8192-token prefill and the
-                131072-token paged decode again with standard-width keys (r = 128,
-                same values), and the thin-key speedup over them next to the
-                byte (decode) or FLOP (prefill) ratio that bounds it.
+  fullkey_control  the batch-16 decode, the 8192-token prefill, the
+                131072-token paged decode and the 4-bit-key decode again with
+                standard-width bf16 keys (r = 128, same values), and the thin-key
+                speedup over them next to the byte (decode) or FLOP (prefill)
+                ratio that bounds it.
 """
 from __future__ import annotations
 
@@ -163,22 +164,30 @@ def prefill_result(name, spec, dev, steps, warmup):
     }
 
 
-def append_result(name, B, Hkv, T, r, dv, fp8, dev, steps, warmup):
-    """tk_cache_append of T new tokens per (sequence, KV head) into a contiguous cache."""
+APPEND_CASES = {"cache_append_s8192": (4, 8192, "bf16"), "cache_append_fp8_s8192": (4, 8192, "fp8"),
+                "cache_append_int4_s8192": (4, 8192, "int4"), "cache_append_decode_b16": (16, 1, "bf16")}
+
+
+def append_result(name, B, Hkv, T, r, dv, kdt, dev, steps, warmup):
+    """tk_cache_append of T new tokens per (sequence, KV head) into a contiguous cache
+    with bf16, fp8 or 4-bit keys (``kdt``)."""
     import torch
     from paper_2603_04427_amd import prepare_cache_append
     from synth import normal, stream_key
 
     kn = normal(stream_key(20, 0), B * Hkv * T * r, device=dev).view(B, Hkv, T, r).to(torch.bfloat16)
     vn = normal(stream_key(20, 1), B * Hkv * T * dv, device=dev).view(B, Hkv, T, dv).to(torch.bfloat16)
-    kc = torch.zeros(B, Hkv, T, r, dtype=torch.uint8 if fp8 else torch.bfloat16, device=dev)
+    quant = kdt != "bf16"
+    kc = torch.zeros(B, Hkv, T, r // 2 if kdt == "int4" else r, dtype=torch.uint8 if quant else torch.bfloat16,
+                     device=dev)
     vc = torch.zeros(B, Hkv, T, dv, dtype=torch.bfloat16, device=dev)
-    ks = torch.zeros(B, Hkv, T, dtype=torch.float32, device=dev) if fp8 else None
+    ks = torch.zeros(B, Hkv, T, dtype=torch.float32, device=dev) if quant else None
     pos = torch.zeros(B, dtype=torch.int32, device=dev)
     call = prepare_cache_append(kn, vn, pos, kc, vc, k_scale=ks)
     wall, ev = time_calls([call], steps, warmup)
     tokens = B * Hkv * T
-    nbytes = tokens * (r * 2 + dv * 2) + B * 4 + tokens * ((r + 4) if fp8 else r * 2) + tokens * dv * 2
+    key_out = {"bf16": r * 2, "fp8": r + 4, "int4": r // 2 + 4}[kdt]
+    nbytes = tokens * (r * 2 + dv * 2) + B * 4 + tokens * key_out + tokens * dv * 2
     del kn, vn, kc, vc, ks, call
     torch.cuda.empty_cache()
     from paper_2603_04427_amd import accounting as acc
@@ -202,9 +211,10 @@ def cpu_baseline(spec, budget_s: float):
 
     d = make_decode(spec, device="cpu")
     nbytes = acc.decode_bytes(spec.lens, spec.h_q, spec.h_kv, spec.r, spec.d_v, spec.k_dtype)
+    keys = oracle.Int4(d["k_logical"]) if spec.k_dtype == "int4" else d["k_logical"]
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.decode(d["q"], d["k_logical"], d["v_logical"], d["ctx_lens"], scale=spec.softmax_scale,
+        oracle.decode(d["q"], keys, d["v_logical"], d["ctx_lens"], scale=spec.softmax_scale,
                       k_scale=d["k_scale_logical"])
         reps += 1
         el = time.perf_counter() - t0
@@ -238,7 +248,8 @@ def main():
               "GPUs. Run with --gpus 1.", file=sys.stderr)
         sys.exit(2)
     import torch
-    from synth import FULLKEY, WORKLOADS
+    from synth import FULLKEY, INT4KEY, WORKLOADS
+    workloads = {**WORKLOADS, **INT4KEY}
 
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
@@ -248,10 +259,8 @@ def main():
         copy_calibration(args.copy_calibration, dev)
         return
     if args.only and args.only.startswith("cache_append"):
-        cases = {"cache_append_s8192": (4, 8192, False), "cache_append_fp8_s8192": (4, 8192, True),
-                 "cache_append_decode_b16": (16, 1, False)}
-        B, T, fp8 = cases[args.only]
-        res = append_result(args.only, B, 8, T, 32, 128, fp8, dev, args.steps, args.warmup)
+        B, T, kdt = APPEND_CASES[args.only]
+        res = append_result(args.only, B, 8, T, 32, 128, kdt, dev, args.steps, args.warmup)
         print(json.dumps({"metric": "cache append HBM GB/s", "value": res["value"], "unit": "GB/s", "n_gpus": 1,
                           "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_call"],
                           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
@@ -262,7 +271,7 @@ def main():
     results = {}
     order = [main_name] if (args.no_secondary or args.only) else \
         [main_name] + [n for n in ("mistral_prefill_s8192", "longctx_paged_decode", "fp8key_decode",
-                                   "gpt2_prefill_f32") if n != main_name]
+                                   "int4key_decode", "gpt2_prefill_f32") if n != main_name]
     def run(name, spec, main=False):
         print(f"bench: timing {name}", file=sys.stderr, flush=True)
         if hasattr(spec, "ctx"):
@@ -279,17 +288,17 @@ def main():
         return res
 
     for name in order:
-        results[name] = run(name, WORKLOADS[name], main=name == main_name)
+        results[name] = run(name, workloads[name], main=name == main_name)
     fullkey = []
     if not (args.no_fullkey or args.only or args.no_secondary):
         from paper_2603_04427_amd import accounting as acc
         for name, spec in FULLKEY.items():
             thin = results[name[:-len("_fullkey")]]
             full = run(name, spec)
-            tspec = WORKLOADS[name[:-len("_fullkey")]]
+            tspec = workloads[name[:-len("_fullkey")]]
             if hasattr(spec, "ctx"):
-                ideal = acc.decode_bytes(spec.lens, spec.h_q, spec.h_kv, spec.r, spec.d_v) / \
-                    acc.decode_bytes(tspec.lens, tspec.h_q, tspec.h_kv, tspec.r, tspec.d_v)
+                ideal = acc.decode_bytes(spec.lens, spec.h_q, spec.h_kv, spec.r, spec.d_v, spec.k_dtype) / \
+                    acc.decode_bytes(tspec.lens, tspec.h_q, tspec.h_kv, tspec.r, tspec.d_v, tspec.k_dtype)
             else:
                 ideal = (spec.r + spec.d_v) / (tspec.r + tspec.d_v)
             full["thin_key_speedup"] = round(full["roofline"]["kernel_ms"] / thin["roofline"]["kernel_ms"], 3)
@@ -297,18 +306,18 @@ def main():
             fullkey.append(full)
     appends = []
     if not (args.only or args.no_secondary):
-        for name, B, T, fp8 in (("cache_append_s8192", 4, 8192, False), ("cache_append_fp8_s8192", 4, 8192, True),
-                                ("cache_append_decode_b16", 16, 1, False)):
+        for name, (B, T, kdt) in APPEND_CASES.items():
             print(f"bench: timing {name}", file=sys.stderr, flush=True)
-            appends.append(append_result(name, B, 8, T, 32, 128, fp8, dev, max(10, args.steps // 10),
+            appends.append(append_result(name, B, 8, T, 32, 128, kdt, dev, max(10, args.steps // 10),
                                          args.warmup))
     m = results[main_name]
-    spec = WORKLOADS[main_name]
+    spec = workloads[main_name]
     is_decode = hasattr(spec, "ctx")
     line = {
         "metric": METRIC, "value": m["value"], "unit": m["unit"], "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": m["ms_per_call"], "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16" if (not is_decode or spec.k_dtype == "bf16") else "fp8-keys/bf16",
+        "vs_baseline": None, "dtype": "bf16" if (not is_decode or spec.k_dtype == "bf16") else
+        f"{spec.k_dtype}-keys/bf16",
         "data": "synthetic (seeded N(0,1) draws shaped like the paper's Mistral-7B decode)",
         "config": ({"workload": main_name, "batch": spec.batch, "h_q": spec.h_q, "h_kv": spec.h_kv,
                     "ctx": spec.ctx, "r": spec.r, "d_v": spec.d_v, "k_dtype": spec.k_dtype,

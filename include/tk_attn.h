@@ -47,7 +47,9 @@ typedef enum {
 typedef enum {
     TK_F32 = 0,
     TK_BF16 = 1,
-    TK_FP8_E4M3 = 2  /* OCP E4M3FN codes (bias 7, no infinities, max 448) */
+    TK_FP8_E4M3 = 2, /* OCP E4M3FN codes (bias 7, no infinities, max 448) */
+    TK_INT4 = 3      /* 4-bit integer key codes -7 .. 7, stored excess-8 (nibble c + 8),
+                        two per byte, the even entry in the low nibble */
 } tk_dtype;
 
 /*
@@ -101,9 +103,10 @@ size_t tk_attn_decode_workspace_bytes(int batch, int H_q, int H_kv, int max_ctx,
  *       block_size must be a power of two >= 64 and
  *       max_ctx <= block_size * max_blocks_per_seq. A table entry outside
  *       [0, num_blocks) is never dereferenced: that sequence's output is NaN.
- *   k_dtype: TK_BF16 keys, or TK_FP8_E4M3 key codes (uint8) with one fp32 scale
- *       per (token, KV head) in k_scale (the key row is code * scale).
- *       k_scale must be NULL for bf16 keys.
+ *   k_dtype: TK_BF16 keys; TK_FP8_E4M3 key codes (r bytes per row); or TK_INT4
+ *       4-bit key codes (r/2 bytes per row, so K_cache rows are r/2 bytes wide).
+ *       Quantised keys come with one fp32 scale per (token, KV head) in k_scale
+ *       (the key row is code * scale); k_scale must be NULL for bf16 keys.
  *   V_cache is always bf16.
  *   workspace: device memory of at least
  *       tk_attn_decode_workspace_bytes(batch, H_q, H_kv, max_ctx, d_v) bytes,
@@ -140,7 +143,9 @@ tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache
  *       the way in (the composition with quantisation of Sec. 6): its scale is
  *       max|k| / 448 over the row's r entries (1.0 for an all-zero row), stored in
  *       k_scale, and each entry becomes the OCP E4M3 code of k / scale rounded to
- *       nearest-even; both steps in fp32 with IEEE division.
+ *       nearest-even; both steps in fp32 with IEEE division. TK_INT4 does the same
+ *       with scale max|k| / 7 and code k / scale rounded half-to-even and clipped
+ *       to [-7, 7], stored excess-8 (see tk_dtype).
  * A token whose position is negative or not below the capacity, or whose block
  * table entry lies outside [0, num_blocks), is not written (nothing else is
  * touched). Tokens of one call must land on distinct positions. V_cache rows and

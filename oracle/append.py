@@ -13,6 +13,11 @@ with round-to-nearest-even, every step in fp32 (IEEE division), so that the
 integer codes are decided in the same precision as on the GPU. The rounding to
 E4M3 uses torch's float8_e4m3fn conversion as a library step.
 
+4-bit integer keys: per key row, scale = max|k| / 7 (1 for an all-zero row) and
+code c = k / scale rounded half-to-even and clipped to [-7, 7], in fp32; stored
+excess-8 (nibble c + 8), entry 2j in the low and entry 2j + 1 in the high nibble
+of byte j.
+
 Nothing here is shared with the GPU library; only the tests use it.
 """
 from __future__ import annotations
@@ -34,19 +39,34 @@ def quantize_rows(k: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
     return codes, scale
 
 
+def quantize_rows_int4(k: torch.Tensor) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Per-row (last axis, even length) packed 4-bit codes (uint8 [..., r / 2]) and
+    fp32 scales of fp32 rows ``k``."""
+    k = k.to(torch.float32)
+    amax = k.abs().amax(dim=-1)
+    scale = torch.where(amax > 0, amax / torch.tensor(7.0, dtype=torch.float32), torch.ones_like(amax))
+    c = torch.round(k / scale.unsqueeze(-1)).clamp(-7, 7).to(torch.int32) + 8  # round: half to even
+    packed = (c[..., 0::2] | (c[..., 1::2] << 4)).to(torch.uint8)
+    return packed, scale
+
+
 def cache_append(k_new: torch.Tensor, v_new: torch.Tensor, positions: torch.Tensor, k_cache: torch.Tensor,
                  v_cache: torch.Tensor, k_scale: Optional[torch.Tensor] = None,
-                 block_table: Optional[torch.Tensor] = None, block_size: int = 0):
+                 block_table: Optional[torch.Tensor] = None, block_size: int = 0, k_format: str = "auto"):
     """Returns copies of (k_cache, v_cache, k_scale) with the new rows written.
 
     k_new [B, Hkv, T, r], v_new [B, Hkv, T, dv] (bf16); positions [B] int; caches on
-    the CPU. ``k_cache`` of dtype uint8 means E4M3 codes with ``k_scale``."""
+    the CPU. ``k_cache`` of dtype uint8 holds E4M3 codes [.., r] or, with
+    k_format="int4", packed 4-bit codes [.., r / 2], with ``k_scale``."""
     k_cache, v_cache = k_cache.clone(), v_cache.clone()
     k_scale = None if k_scale is None else k_scale.clone()
     B, Hkv, T, r = k_new.shape
     fp8 = k_cache.dtype == torch.uint8
     if fp8:
-        codes, scales = quantize_rows(k_new.to(torch.float32))
+        if k_format == "int4":
+            codes, scales = quantize_rows_int4(k_new.to(torch.float32))
+        else:
+            codes, scales = quantize_rows(k_new.to(torch.float32))
     if block_table is None:
         capacity = k_cache.shape[2]
     else:

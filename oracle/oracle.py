@@ -3,7 +3,8 @@
 TEST INFRASTRUCTURE ONLY: imported by the tests, the smoke check and the
 CPU-baseline leg of the benchmark, never by the GPU library. It shares no code
 with the GPU path; inputs are passed exactly as the GPU receives them (fp32,
-bf16 bit patterns, E4M3 codes with fp32 scales) and widened inside the oracle.
+bf16 bit patterns, E4M3 or packed 4-bit integer codes with fp32 scales) and
+widened inside the oracle.
 
 Each call is the plain definition of thin-key attention (Sec. 2.1, Eq. 4): see
 the header of ``tk_oracle.c``.
@@ -20,8 +21,20 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "tk_oracle.c")
 _LIB = os.path.join(_HERE, "libtkoracle.so")
 
-F64, F32, BF16, E4M3 = 0, 1, 2, 3
+F64, F32, BF16, E4M3, INT4 = 0, 1, 2, 3, 4
 _lib = None
+
+
+class Int4:
+    """Marks a uint8 tensor [..., r / 2] as packed 4-bit key codes (excess-8, low
+    nibble first); the key entry is (nibble - 8) * its row's scale."""
+
+    def __init__(self, packed: torch.Tensor):
+        self.packed = packed
+
+    @property
+    def shape(self):  # shape in key entries
+        return (*self.packed.shape[:-1], self.packed.shape[-1] * 2)
 
 
 def build(force: bool = True) -> str:
@@ -50,13 +63,18 @@ def lib():
         L.tko_decode.restype = i
         L.tko_e4m3_value.argtypes = [ctypes.c_uint8]
         L.tko_e4m3_value.restype = d
+        L.tko_int4_value.argtypes = [vp, ctypes.c_size_t]
+        L.tko_int4_value.restype = d
         L.tko_max_threads.restype = i
         _lib = L
     return _lib
 
 
-def _typed(x: torch.Tensor):
+def _typed(x):
     """(pointer, dtype code, keep-alive tensor) for a CPU tensor."""
+    if isinstance(x, Int4):
+        p = x.packed.detach().cpu().contiguous().view(torch.uint8)
+        return ctypes.c_void_p(p.data_ptr()), INT4, p
     x = x.detach().cpu().contiguous()
     if x.dtype == torch.float64:
         code = F64
@@ -75,6 +93,12 @@ def _typed(x: torch.Tensor):
 def e4m3_value(code: int) -> float:
     """The oracle's decode of one OCP E4M3FN code."""
     return lib().tko_e4m3_value(code)
+
+
+def int4_value(packed_row: torch.Tensor, i: int) -> float:
+    """The oracle's decode of entry i of a packed 4-bit code row."""
+    p = packed_row.detach().cpu().contiguous().view(torch.uint8)
+    return lib().tko_int4_value(ctypes.c_void_p(p.data_ptr()), i)
 
 
 def max_threads() -> int:

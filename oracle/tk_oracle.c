@@ -19,8 +19,9 @@
  *     O[b,h,i,:] = sum_j (p_j / l) * V[b,g,j,:]
  *
  * Everything is evaluated in fp64 from the exact widening of the inputs the GPU
- * receives (fp32, bf16, or OCP E4M3FN key codes times an fp32 per-token scale,
- * which is the composition with quantisation the discussion in Sec. 6 proposes).
+ * receives (fp32, bf16, or OCP E4M3FN or 4-bit integer key codes times an fp32
+ * per-token scale, which is the composition with quantisation the discussion in
+ * Sec. 6 proposes).
  * Two passes (maximum, then sums) - no online rescaling, no blocking, no
  * splitting. Paged caches are read by explicit index through the block table.
  * A row with no visible key (decode with ctx_len 0) yields zeros.
@@ -39,7 +40,7 @@
 #include <omp.h>
 #endif
 
-enum { TKO_F64 = 0, TKO_F32 = 1, TKO_BF16 = 2, TKO_E4M3 = 3 };
+enum { TKO_F64 = 0, TKO_F32 = 1, TKO_BF16 = 2, TKO_E4M3 = 3, TKO_INT4 = 4 };
 
 /* OCP 8-bit floating point, E4M3FN: 1 sign bit, 4 exponent bits (bias 7),
  * 3 mantissa bits; exponent field 0 is subnormal (2^-6 * m/8); no infinities;
@@ -53,6 +54,15 @@ double tko_e4m3_value(uint8_t code) {
     else
         mag = ldexp(1.0 + (double)m / 8.0, e - 7);
     return s ? -mag : mag;
+}
+
+/* 4-bit integer key codes, excess-8: the nibble n holds the integer n - 8
+ * (-7 .. 7 in use); entry i of a row is nibble i % 2 (low nibble first) of byte
+ * i / 2. Rows have an even number of entries, so they start on byte boundaries. */
+double tko_int4_value(const uint8_t* codes, size_t i) {
+    const uint8_t byte = codes[i >> 1];
+    const int n = (i & 1) ? (byte >> 4) : (byte & 15);
+    return (double)(n - 8);
 }
 
 /* bfloat16 is the upper half of an IEEE binary32. */
@@ -70,6 +80,7 @@ static double ld(const void* p, int dt, size_t i) {
         case TKO_F32: return (double)((const float*)p)[i];
         case TKO_BF16: return bf16_value(((const uint16_t*)p)[i]);
         case TKO_E4M3: return tko_e4m3_value(((const uint8_t*)p)[i]);
+        case TKO_INT4: return tko_int4_value((const uint8_t*)p, i);
         default: return NAN;
     }
 }

@@ -7,7 +7,8 @@ Two kinds of figures live here:
   (Sec. 3, Exp. 7b), and the decode bandwidth model of Eq. 10 (Sec. 4.2).
 * The algorithmic work of one kernel call, used as the numerator of achieved
   GB/s and TFLOP/s: decode moves every visible key row (r elements of the key
-  dtype, plus one fp32 scale per row for fp8 keys) and every value row (d_v
+  dtype, half a byte each for 4-bit keys, plus one fp32 scale per row for
+  quantised keys) and every value row (d_v
   bf16) once per KV head, plus the queries, outputs, lengths and block table;
   causal prefill performs 2 (r + d_v) FLOPs for each (query head, visible key)
   pair, the diagonal included, with no credit for masked work.
@@ -52,14 +53,14 @@ def decode_speedup(w: float, c_kv: float, w_thin: float, c_kv_thin: float, batch
 
 # ---------------------------------------------------------------- kernel work
 
-KEY_BYTES = {"bf16": 2, "fp8": 1, "f32": 4}
+KEY_BYTES = {"bf16": 2, "fp8": 1, "int4": 0.5, "f32": 4}
 
 
 def decode_bytes(ctx_lens: Sequence[int], h_q: int, h_kv: int, r: int, d_v: int,
                  k_dtype: str = "bf16", paged_blocks_per_seq: Optional[int] = None) -> int:
     """Algorithmic bytes of one decode call (bf16 queries, values and outputs)."""
     kb = KEY_BYTES[k_dtype]
-    per_token = h_kv * (r * kb + (4 if k_dtype == "fp8" else 0) + d_v * 2)
+    per_token = h_kv * (int(r * kb) + (4 if k_dtype in ("fp8", "int4") else 0) + d_v * 2)
     total = sum(int(L) for L in ctx_lens) * per_token
     B = len(ctx_lens)
     total += B * h_q * r * 2 + B * h_q * d_v * 2 + B * 4

@@ -17,7 +17,7 @@ import torch
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtkattn.so")
 
 TK_OK, TK_ERR_INVALID_ARG, TK_ERR_UNSUPPORTED, TK_ERR_WORKSPACE, TK_ERR_HIP = 0, 1, 2, 3, 4
-TK_F32, TK_BF16, TK_FP8_E4M3 = 0, 1, 2
+TK_F32, TK_BF16, TK_FP8_E4M3, TK_INT4 = 0, 1, 2, 3
 
 # exported functions and their ctypes signatures (kept in step with include/tk_attn.h)
 _vp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
@@ -134,28 +134,40 @@ def tk_attn_decode_workspace_bytes(batch: int, H_q: int, H_kv: int, max_ctx: int
     return int(lib().tk_attn_decode_workspace_bytes(batch, H_q, H_kv, max_ctx, d_v))
 
 
+def _key_format(K_cache: torch.Tensor, r: int) -> int:
+    """bf16 rows, E4M3 codes (uint8 / float8_e4m3fn, r per row) or packed 4-bit codes (uint8, r/2 per row)."""
+    if K_cache.dtype == torch.bfloat16:
+        return TK_BF16
+    if K_cache.shape[-1] == r:
+        return TK_FP8_E4M3
+    if K_cache.dtype == torch.uint8 and K_cache.shape[-1] * 2 == r:
+        return TK_INT4
+    raise ValueError(f"K_cache rows of {K_cache.shape[-1]} {K_cache.dtype} do not hold {r} key entries")
+
+
 def prepare_decode(Q: torch.Tensor, K_cache: torch.Tensor, V_cache: torch.Tensor, ctx_lens: torch.Tensor,
                    max_ctx: Optional[int] = None, scale: float = 0.0, k_scale: Optional[torch.Tensor] = None,
                    block_table: Optional[torch.Tensor] = None, block_size: int = 0,
                    workspace: Optional[torch.Tensor] = None, O: Optional[torch.Tensor] = None,
                    stream=None) -> PreparedCall:
-    """One decode step, marshalled. Q [B,Hq,r] bf16; K_cache bf16 or uint8 E4M3 codes (with k_scale fp32);
-    contiguous [B,Hkv,max_ctx,*] or paged [nblk,Hkv,bs,*] with block_table [B, mb] int32."""
+    """One decode step, marshalled. Q [B,Hq,r] bf16; K_cache bf16, uint8 E4M3 codes or uint8 packed 4-bit
+    codes [.., r/2] (quantised keys with k_scale fp32); contiguous [B,Hkv,max_ctx,*] or paged
+    [nblk,Hkv,bs,*] with block_table [B, mb] int32."""
     _check(Q, "Q", (torch.bfloat16,), 3)
     _check(K_cache, "K_cache", (torch.bfloat16, torch.uint8, torch.float8_e4m3fn), 4)
     _check(V_cache, "V_cache", (torch.bfloat16,), 4)
     _check(ctx_lens, "ctx_lens", (torch.int32,), 1)
     B, Hq, r = Q.shape
     Hkv, dv = V_cache.shape[1], V_cache.shape[3]
-    fp8 = K_cache.dtype != torch.bfloat16
-    if fp8:
+    kf = _key_format(K_cache, r)
+    if kf != TK_BF16:
         if k_scale is None:
-            raise ValueError("fp8 keys need k_scale")
+            raise ValueError("quantised keys need k_scale")
         _check(k_scale, "k_scale", (torch.float32,), 3)
         K_cache = K_cache.view(torch.uint8)
     elif k_scale is not None:
-        raise ValueError("k_scale is only for fp8 keys")
-    if K_cache.shape[1] != Hkv or K_cache.shape[3] != r or K_cache.shape[:3] != V_cache.shape[:3]:
+        raise ValueError("k_scale is only for quantised keys")
+    if K_cache.shape[1] != Hkv or K_cache.shape[:3] != V_cache.shape[:3]:
         raise ValueError(f"cache shapes K{tuple(K_cache.shape)} V{tuple(V_cache.shape)} do not match r={r}")
     if k_scale is not None and tuple(k_scale.shape) != tuple(K_cache.shape[:3]):
         raise ValueError("k_scale must be [*, Hkv, tokens]")
@@ -189,7 +201,7 @@ def prepare_decode(Q: torch.Tensor, K_cache: torch.Tensor, V_cache: torch.Tensor
         O = torch.empty(B, Hq, dv, dtype=torch.bfloat16, device=Q.device)
     _check(O, "O", (torch.bfloat16,), 3)
     args = (_ptr(Q), _ptr(K_cache), _ptr(V_cache), _ptr(O), B, Hq, Hkv, _ptr(ctx_lens), int(max_ctx), r, dv,
-            float(scale), TK_FP8_E4M3 if fp8 else TK_BF16, _ptr(k_scale), _ptr(block_table), int(block_size),
+            float(scale), kf, _ptr(k_scale), _ptr(block_table), int(block_size),
             int(mb), int(nblk), _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
     return PreparedCall("tk_attn_decode", args, (Q, K_cache, V_cache, ctx_lens, k_scale, block_table, workspace, O))
 
@@ -199,8 +211,9 @@ def tk_attn_decode(Q: torch.Tensor, K_cache: torch.Tensor, V_cache: torch.Tensor
                    block_table: Optional[torch.Tensor] = None, block_size: int = 0,
                    workspace: Optional[torch.Tensor] = None, O: Optional[torch.Tensor] = None,
                    stream=None) -> torch.Tensor:
-    """One decode step. Q [B,Hq,r] bf16; K_cache bf16 or uint8 E4M3 codes (with k_scale fp32);
-    contiguous [B,Hkv,max_ctx,*] or paged [nblk,Hkv,bs,*] with block_table [B, mb] int32.
+    """One decode step. Q [B,Hq,r] bf16; K_cache bf16, uint8 E4M3 codes or uint8 packed 4-bit codes
+    [.., r/2] (quantised keys with k_scale fp32); contiguous [B,Hkv,max_ctx,*] or paged [nblk,Hkv,bs,*]
+    with block_table [B, mb] int32.
     A workspace passed in must have been zeroed before its first use (see include/tk_attn.h)."""
     return prepare_decode(Q, K_cache, V_cache, ctx_lens, max_ctx, scale, k_scale, block_table, block_size,
                           workspace, O, stream)()
@@ -212,7 +225,8 @@ def prepare_cache_append(K_new: torch.Tensor, V_new: torch.Tensor, positions: to
                          stream=None) -> PreparedCall:
     """Append marshalled. K_new [B,Hkv,T,r], V_new [B,Hkv,T,dv] bf16; positions [B] int32; caches as for
     decode: contiguous [B,Hkv,max_ctx,*] or paged [nblk,Hkv,bs,*] with block_table [B, mb] int32. A uint8 /
-    float8_e4m3fn K_cache (with k_scale fp32) receives E4M3 codes quantised per row."""
+    float8_e4m3fn K_cache with r entries per row receives E4M3 codes, a uint8 K_cache with r/2 bytes per
+    row packed 4-bit codes, each quantised per row with its scale written to k_scale (fp32)."""
     _check(K_new, "K_new", (torch.bfloat16,), 4)
     _check(V_new, "V_new", (torch.bfloat16,), 4)
     _check(positions, "positions", (torch.int32,), 1)
@@ -223,16 +237,15 @@ def prepare_cache_append(K_new: torch.Tensor, V_new: torch.Tensor, positions: to
     if tuple(V_new.shape[:3]) != (B, Hkv, T) or positions.shape[0] != B:
         raise ValueError(f"shape mismatch K_new{tuple(K_new.shape)} V_new{tuple(V_new.shape)} "
                          f"positions{tuple(positions.shape)}")
-    fp8 = K_cache.dtype != torch.bfloat16
-    if fp8:
+    kf = _key_format(K_cache, r)
+    if kf != TK_BF16:
         if k_scale is None:
-            raise ValueError("fp8 keys need k_scale")
+            raise ValueError("quantised keys need k_scale")
         _check(k_scale, "k_scale", (torch.float32,), 3)
         K_cache = K_cache.view(torch.uint8)
     elif k_scale is not None:
-        raise ValueError("k_scale is only for fp8 keys")
-    if K_cache.shape[1] != Hkv or K_cache.shape[3] != r or K_cache.shape[:3] != V_cache.shape[:3] \
-            or V_cache.shape[3] != dv:
+        raise ValueError("k_scale is only for quantised keys")
+    if K_cache.shape[1] != Hkv or K_cache.shape[:3] != V_cache.shape[:3] or V_cache.shape[3] != dv:
         raise ValueError(f"cache shapes K{tuple(K_cache.shape)} V{tuple(V_cache.shape)} do not match the rows")
     if k_scale is not None and tuple(k_scale.shape) != tuple(K_cache.shape[:3]):
         raise ValueError("k_scale must be [*, Hkv, tokens]")
@@ -246,7 +259,7 @@ def prepare_cache_append(K_new: torch.Tensor, V_new: torch.Tensor, positions: to
             raise ValueError("block_table must be [B, mb] and block_size the cache's slot dimension")
         max_ctx, mb, nblk = 0, block_table.shape[1], K_cache.shape[0]
     args = (_ptr(K_new), _ptr(V_new), B, Hkv, T, r, dv, _ptr(positions), _ptr(K_cache), _ptr(V_cache),
-            int(max_ctx), TK_FP8_E4M3 if fp8 else TK_BF16, _ptr(k_scale), _ptr(block_table), int(block_size),
+            int(max_ctx), kf, _ptr(k_scale), _ptr(block_table), int(block_size),
             int(mb), int(nblk), _stream(stream))
     return PreparedCall("tk_cache_append", args, (K_new, V_new, positions, k_scale, block_table, K_cache))
 

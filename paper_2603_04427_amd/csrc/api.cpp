@@ -23,6 +23,8 @@ int log2_exact(int x) {
 
 constexpr long kMaxGrid = 65535;
 
+int key_format(tk_dtype k) { return k == TK_FP8_E4M3 ? 1 : (k == TK_INT4 ? 2 : 0); }
+
 }  // namespace
 
 extern "C" {
@@ -87,9 +89,10 @@ tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache
                          hipStream_t stream) {
     if (batch < 0 || H_q <= 0 || H_kv <= 0 || max_ctx < 0 || r <= 0 || d_v <= 0) return TK_ERR_INVALID_ARG;
     if (H_q % H_kv != 0) return TK_ERR_INVALID_ARG;
-    if (k_dtype != TK_BF16 && k_dtype != TK_FP8_E4M3) return k_dtype == TK_F32 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
-    const bool fp8 = k_dtype == TK_FP8_E4M3;
-    if (fp8 != (k_scale != nullptr)) return TK_ERR_INVALID_ARG;  // scales iff fp8 keys
+    if (k_dtype != TK_BF16 && k_dtype != TK_FP8_E4M3 && k_dtype != TK_INT4)
+        return k_dtype == TK_F32 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
+    const bool quantised = k_dtype != TK_BF16;
+    if (quantised != (k_scale != nullptr)) return TK_ERR_INVALID_ARG;  // scales iff quantised keys
     const bool paged = block_table != nullptr;
     int bs_log2 = 0;
     if (paged) {
@@ -134,7 +137,7 @@ tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache
     p.qscale = resolve_scale(scale, r) * tk::kLog2e;
     // wide keys leave no registers for 8 heads per workgroup: use groups of 4
     const int hg = (r >= 64 && pl.heads_per_group > 4) ? 4 : pl.heads_per_group;
-    return tk::launch_decode(p, r, d_v, hg, fp8, paged, stream);
+    return tk::launch_decode(p, r, d_v, hg, key_format(k_dtype), paged, stream);
 }
 
 tk_status tk_cache_append(const void* K_new, const void* V_new, int batch, int H_kv, int n_new, int r, int d_v,
@@ -142,9 +145,10 @@ tk_status tk_cache_append(const void* K_new, const void* V_new, int batch, int H
                           float* k_scale, const int32_t* block_table, int block_size, int max_blocks_per_seq,
                           int num_blocks, hipStream_t stream) {
     if (batch < 0 || H_kv <= 0 || n_new < 0 || r <= 0 || d_v <= 0 || max_ctx < 0) return TK_ERR_INVALID_ARG;
-    if (k_dtype != TK_BF16 && k_dtype != TK_FP8_E4M3) return k_dtype == TK_F32 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
-    const bool fp8 = k_dtype == TK_FP8_E4M3;
-    if (fp8 != (k_scale != nullptr)) return TK_ERR_INVALID_ARG;  // scales iff fp8 keys
+    if (k_dtype != TK_BF16 && k_dtype != TK_FP8_E4M3 && k_dtype != TK_INT4)
+        return k_dtype == TK_F32 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
+    const bool quantised = k_dtype != TK_BF16;
+    if (quantised != (k_scale != nullptr)) return TK_ERR_INVALID_ARG;  // scales iff quantised keys
     const bool paged = block_table != nullptr;
     int bs_log2 = 0;
     long capacity = max_ctx;
@@ -180,7 +184,7 @@ tk_status tk_cache_append(const void* K_new, const void* V_new, int batch, int H
     p.bs_log2 = bs_log2;
     p.mb = paged ? max_blocks_per_seq : 0;
     p.num_blocks = paged ? num_blocks : 0;
-    return tk::launch_append(p, r, d_v, fp8, paged, stream);
+    return tk::launch_append(p, r, d_v, key_format(k_dtype), paged, stream);
 }
 
 }  // extern "C"

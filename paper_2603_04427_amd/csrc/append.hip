@@ -1,18 +1,24 @@
 // Cache append for the thin-key / full-value cache: the write that precedes
 // decode. Token t of sequence b and KV head g is stored at cache position
 // positions[b] + t: its r-entry key row (Sec. 2.4, Eq. 9) and its d_v-entry
-// value row. With fp8 keys each key row is quantised on the way in (the
-// composition with quantisation the discussion in Sec. 6 proposes): one fp32
-// scale per row, max|k| / 448 (1 for an all-zero row), and the OCP E4M3 code of
-// k / scale, rounded to nearest-even, both in fp32 with IEEE division.
+// value row. With quantised keys each key row is quantised on the way in (the
+// composition with quantisation the discussion in Sec. 6 proposes), with one
+// fp32 scale per row, both steps in fp32 with IEEE division:
+//  * E4M3: scale max|k| / 448 (1 for an all-zero row), code the OCP E4M3 of
+//    k / scale rounded to nearest-even;
+//  * 4-bit: scale max|k| / 7 (1 for an all-zero row), code k / scale rounded
+//    half-to-even and clipped to [-7, 7], stored excess-8 (nibble code + 8, the
+//    even entry in the low nibble).
 //
 // The kernel is a plain stream: every thread moves one 16-byte slice of a key or
 // value row. The R / 8 threads holding one key row are consecutive lanes, so the
-// row maximum of the fp8 path is a butterfly over those lanes.
+// row maximum of the quantised paths is a butterfly over those lanes.
 #include "tk_device.hpp"
 #include "tk_internal.hpp"
 
 #include <math.h>
+
+#include <type_traits>
 
 namespace tk {
 
@@ -47,7 +53,7 @@ __device__ __forceinline__ uint32_t e4m3_rne(float x) {
 
 // Grid: x covers the 16-byte slices of one (sequence, KV head)'s new rows, y is
 // the (sequence, KV head) pair, so a thread's token index is a shift.
-template <int R, int DV, bool FP8, bool PAGED>
+template <int R, int DV, int KF, bool PAGED>
 __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendParams p) {
     constexpr int KL = R / 8;   // threads per key row (8 entries each)
     constexpr int VL = DV / 8;  // threads per value row
@@ -78,7 +84,7 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendPara
         const int t = i / KL, slice = i % KL;
         const long row = cache_row(t);
         const uint4 w = *(const uint4*)(kn + (size_t)i * 8);
-        if constexpr (FP8) {
+        if constexpr (KF != kKeyBF16) {
             const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
             float f[8];
             float amax = 0.f;
@@ -90,13 +96,27 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendPara
             }
 #pragma unroll
             for (int o = KL / 2; o >= 1; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
-            const float scale = amax > 0.f ? amax / 448.f : 1.f;
-            uint32_t code[2] = {0u, 0u};
+            if constexpr (KF == kKeyE4M3) {
+                const float scale = amax > 0.f ? amax / 448.f : 1.f;
+                uint32_t code[2] = {0u, 0u};
 #pragma unroll
-            for (int j = 0; j < 8; ++j) code[j >> 2] |= e4m3_rne(f[j] / scale) << (8 * (j & 3));
-            if (row >= 0) {
-                *(uint2*)(p.kc + row * R + slice * 8) = make_uint2(code[0], code[1]);
-                if (slice == 0) p.ks[row] = scale;
+                for (int j = 0; j < 8; ++j) code[j >> 2] |= e4m3_rne(f[j] / scale) << (8 * (j & 3));
+                if (row >= 0) {
+                    *(uint2*)(p.kc + row * R + slice * 8) = make_uint2(code[0], code[1]);
+                    if (slice == 0) p.ks[row] = scale;
+                }
+            } else {
+                const float scale = amax > 0.f ? amax / 7.f : 1.f;
+                uint32_t code = 0u;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    const float c = fminf(fmaxf(__builtin_rintf(f[j] / scale), -7.f), 7.f);  // rint: half to even
+                    code |= (uint32_t)((int)c + 8) << (4 * j);
+                }
+                if (row >= 0) {
+                    *(uint32_t*)(p.kc + row * (R / 2) + slice * 4) = code;
+                    if (slice == 0) p.ks[row] = scale;
+                }
             }
         } else {
             if (row >= 0) *(uint4*)(p.kc + (row * R + slice * 8) * 2) = w;
@@ -110,41 +130,43 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendPara
 }
 
 template <int R, int DV>
-hipError_t run(const AppendParams& p, bool fp8, bool paged, hipStream_t st) {
+hipError_t run(const AppendParams& p, int kf, bool paged, hipStream_t st) {
     const long work = (long)p.T * (DV / 8 > R / 8 ? DV / 8 : R / 8);
     long bx = (work + kAppendThreads - 1) / kAppendThreads;
     bx = bx < 1024 ? bx : 1024;  // grid-stride beyond that
     const dim3 grid((unsigned)bx, (unsigned)(p.B * p.Hkv)), block(kAppendThreads);
-    if (fp8) {
+    auto launch = [&](auto kf_c) {
+        constexpr int KF = decltype(kf_c)::value;
         if (paged)
-            hipLaunchKernelGGL((append_kernel<R, DV, true, true>), grid, block, 0, st, p);
+            hipLaunchKernelGGL((append_kernel<R, DV, KF, true>), grid, block, 0, st, p);
         else
-            hipLaunchKernelGGL((append_kernel<R, DV, true, false>), grid, block, 0, st, p);
-    } else {
-        if (paged)
-            hipLaunchKernelGGL((append_kernel<R, DV, false, true>), grid, block, 0, st, p);
-        else
-            hipLaunchKernelGGL((append_kernel<R, DV, false, false>), grid, block, 0, st, p);
+            hipLaunchKernelGGL((append_kernel<R, DV, KF, false>), grid, block, 0, st, p);
+    };
+    switch (kf) {
+        case kKeyBF16: launch(std::integral_constant<int, kKeyBF16>{}); break;
+        case kKeyE4M3: launch(std::integral_constant<int, kKeyE4M3>{}); break;
+        case kKeyInt4: launch(std::integral_constant<int, kKeyInt4>{}); break;
+        default: return hipErrorInvalidValue;
     }
     return hipGetLastError();
 }
 
 template <int R>
-hipError_t by_dv(const AppendParams& p, int DV, bool fp8, bool paged, hipStream_t st) {
-    if (DV == 64) return run<R, 64>(p, fp8, paged, st);
-    if (DV == 128) return run<R, 128>(p, fp8, paged, st);
+hipError_t by_dv(const AppendParams& p, int DV, int kf, bool paged, hipStream_t st) {
+    if (DV == 64) return run<R, 64>(p, kf, paged, st);
+    if (DV == 128) return run<R, 128>(p, kf, paged, st);
     return hipErrorInvalidValue;
 }
 
 }  // namespace
 
-tk_status launch_append(const AppendParams& p, int R, int DV, bool fp8, bool paged, hipStream_t st) {
+tk_status launch_append(const AppendParams& p, int R, int DV, int kf, bool paged, hipStream_t st) {
     hipError_t e;
     switch (R) {
-        case 16: e = by_dv<16>(p, DV, fp8, paged, st); break;
-        case 32: e = by_dv<32>(p, DV, fp8, paged, st); break;
-        case 64: e = by_dv<64>(p, DV, fp8, paged, st); break;
-        case 128: e = by_dv<128>(p, DV, fp8, paged, st); break;
+        case 16: e = by_dv<16>(p, DV, kf, paged, st); break;
+        case 32: e = by_dv<32>(p, DV, kf, paged, st); break;
+        case 64: e = by_dv<64>(p, DV, kf, paged, st); break;
+        case 128: e = by_dv<128>(p, DV, kf, paged, st); break;
         default: return TK_ERR_UNSUPPORTED;
     }
     if (e == hipErrorInvalidValue) return TK_ERR_UNSUPPORTED;

@@ -26,6 +26,8 @@
 
 #include <math.h>
 
+#include <type_traits>
+
 #ifndef TK_DECODE_TARGET_GROUPS
 #define TK_DECODE_TARGET_GROUPS 256
 #endif
@@ -56,6 +58,11 @@ __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_
     const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
     return make_uint4(v[0], v[1], v[2], v[3]);
 }
+__device__ __forceinline__ uint2 buffer_load8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+    return make_uint2(v[0], v[1]);
+}
 __device__ __forceinline__ uint32_t buffer_load4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
 }
@@ -68,13 +75,22 @@ __device__ __forceinline__ int load_uniform(const int32_t* p) {
 // Wait until this thread's outstanding global stores have completed.
 __device__ __forceinline__ void wait_stores() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-template <int R, int DV, int HG, bool FP8, int CH>
+template <int KF>
+struct KeyRow {
+    static constexpr bool SCALED = KF != kKeyBF16;
+    static constexpr int SLICE = KF == kKeyInt4 ? 8 : 16;  // bytes of a key row per lane (one load)
+    static constexpr int EPL = KF == kKeyBF16 ? 8 : 16;    // key entries per lane slice
+    template <int R>
+    static constexpr int bytes() { return KF == kKeyBF16 ? 2 * R : (KF == kKeyE4M3 ? R : R / 2); }
+};
+
+template <int R, int DV, int HG, int KF, int CH>
 struct DecodeShape {
-    static constexpr int KB = FP8 ? 1 : 2;     // bytes per key element
-    static constexpr int ROWB = R * KB;        // bytes per key row
-    static constexpr int LPT = ROWB / 16;      // lanes per key row (one 16-byte slice each)
-    static constexpr int EPL = 16 / KB;        // key elements per lane slice
-    static constexpr int QW = EPL / 2;         // packed bf16 query dwords per head and lane
+    using KR = KeyRow<KF>;
+    static constexpr int ROWB = KR::template bytes<R>();  // bytes per key row
+    static constexpr int LPT = ROWB / KR::SLICE;          // lanes per key row (one slice each)
+    static constexpr int EPL = KR::EPL;                   // key entries per lane slice
+    static constexpr int QW = EPL / 2;                    // packed bf16 query dwords per head and lane
     static constexpr int TPK = 64 / LPT;       // key rows per wave-wide load
     static constexpr int KL = CH / TPK;        // key loads per chunk
     static constexpr int LPV = DV * 2 / 16;    // lanes per value row
@@ -88,22 +104,25 @@ struct DecodeShape {
 // before the current chunk is processed (two register buffers). Chosen so the
 // buffers fit the 256-register budget of two waves per SIMD: 32-token chunks
 // double-buffered where a chunk would otherwise need too many registers.
-template <int R, int DV, int HG, bool FP8>
+template <int R, int DV, int HG, int KF>
 struct DecodeSchedule {
-    static constexpr int kRegs64 = (R * (FP8 ? 1 : 2) / 16) * 4 + (DV / 8) * 4;  // one 64-token buffer
-    static constexpr int kBase = HG * 8 + HG * (FP8 ? 8 : 4) + 2 * HG + 48;
-    static constexpr bool kFits64 = kBase + 2 * kRegs64 + HG * (R * (FP8 ? 1 : 2) / 16) <= 200;
-    static constexpr bool kShort = !kFits64 && 64 / (R * (FP8 ? 1 : 2) / 16) <= 32;
+    using KR = KeyRow<KF>;
+    static constexpr int LPT = KR::template bytes<R>() / KR::SLICE;
+    static constexpr int kRegs64 = KR::template bytes<R>() / 4 + DV / 2;  // one 64-token buffer
+    static constexpr int kBase = HG * 8 + HG * (KR::EPL / 2) + 2 * HG + 48 + (KF == kKeyInt4 ? HG : 0);
+    static constexpr bool kFits64 = kBase + 2 * kRegs64 + HG * LPT <= 200;
+    static constexpr bool kShort = !kFits64 && 64 / LPT <= 32;
     static constexpr int CH = kShort ? 32 : 64;
-    static constexpr bool PIPE = kFits64 || kBase + kRegs64 + HG * (R * (FP8 ? 1 : 2) / 16) <= 200;
+    static constexpr bool PIPE = kFits64 || kBase + kRegs64 + HG * LPT <= 200;
 };
 
-// One chunk of 64 tokens as this lane holds it.
-template <int R, int DV, int HG, bool FP8, int CH>
+// One chunk of CH tokens as this lane holds it.
+template <int R, int DV, int HG, int KF, int CH>
 struct Chunk {
-    using S = DecodeShape<R, DV, HG, FP8, CH>;
-    uint4 k[S::KL];
-    float ks[FP8 ? S::KL : 1];
+    using S = DecodeShape<R, DV, HG, KF, CH>;
+    using KVec = typename std::conditional<KF == kKeyInt4, uint2, uint4>::type;
+    KVec k[S::KL];
+    float ks[KeyRow<KF>::SCALED ? S::KL : 1];
     uint4 v[S::VL];
     int nvalid;  // tokens of the chunk inside the context (0: skip, bad page)
 };
@@ -114,10 +133,10 @@ struct Chunk {
 // per lane, a wave-uniform base, constant offsets per load, no branches.
 // Returns false (and loads nothing) for a block-table entry outside
 // [0, num_blocks).
-template <int R, int DV, int HG, bool FP8, int CH, bool PAGED>
-__device__ __forceinline__ bool load_chunk(Chunk<R, DV, HG, FP8, CH>& c, const DecodeParams& p, int b, int g, int ts,
+template <int R, int DV, int HG, int KF, int CH, bool PAGED>
+__device__ __forceinline__ bool load_chunk(Chunk<R, DV, HG, KF, CH>& c, const DecodeParams& p, int b, int g, int ts,
                                            int avail, int lane) {
-    using S = DecodeShape<R, DV, HG, FP8, CH>;
+    using S = DecodeShape<R, DV, HG, KF, CH>;
     const int nrows = avail - ts < CH ? avail - ts : CH;
     size_t row0;
     if constexpr (PAGED) {
@@ -135,11 +154,16 @@ __device__ __forceinline__ bool load_chunk(Chunk<R, DV, HG, FP8, CH>& c, const D
     const int vgrp = lane / S::LPV, vpart = lane % S::LPV;
     const auto kr = make_rsrc(p.k + row0 * S::ROWB, (uint32_t)(nrows * S::ROWB));
     const auto vr = make_rsrc(p.v + row0 * DV, (uint32_t)(nrows * DV * 2));
-    const uint32_t koff = (uint32_t)(kgrp * S::ROWB + kpart * 16);
+    const uint32_t koff = (uint32_t)(kgrp * S::ROWB + kpart * KeyRow<KF>::SLICE);
     const uint32_t voff = (uint32_t)((vgrp * DV + vpart * 8) * 2);
 #pragma unroll
-    for (int j = 0; j < S::KL; ++j) c.k[j] = buffer_load16(kr, koff, j * S::TPK * S::ROWB);
-    if constexpr (FP8) {
+    for (int j = 0; j < S::KL; ++j) {
+        if constexpr (KF == kKeyInt4)
+            c.k[j] = buffer_load8(kr, koff, j * S::TPK * S::ROWB);
+        else
+            c.k[j] = buffer_load16(kr, koff, j * S::TPK * S::ROWB);
+    }
+    if constexpr (KeyRow<KF>::SCALED) {
         const auto sr = make_rsrc(p.k_scale + row0, (uint32_t)(nrows * 4));
 #pragma unroll
         for (int j = 0; j < S::KL; ++j) c.ks[j] = __uint_as_float(buffer_load4(sr, kgrp * 4, j * S::TPK * 4));
@@ -159,11 +183,11 @@ struct WaveState {
 // Folds one chunk into the wave's state; rows t >= nvalid of the chunk are
 // outside the context (their scores become -inf and their values zero, since
 // cache memory past the context may hold anything).
-template <int R, int DV, int HG, bool FP8, int CH>
-__device__ __forceinline__ void process_chunk(Chunk<R, DV, HG, FP8, CH>& c, int nvalid, WaveState<HG>& st,
-                                              const uint32_t (&qp)[HG][DecodeShape<R, DV, HG, FP8, CH>::QW],
-                                              float qscale, uint16_t* p16, int lane) {
-    using S = DecodeShape<R, DV, HG, FP8, CH>;
+template <int R, int DV, int HG, int KF, int CH>
+__device__ __forceinline__ void process_chunk(Chunk<R, DV, HG, KF, CH>& c, int nvalid, WaveState<HG>& st,
+                                              const uint32_t (&qp)[HG][DecodeShape<R, DV, HG, KF, CH>::QW],
+                                              const float (&qsum)[HG], float qscale, uint16_t* p16, int lane) {
+    using S = DecodeShape<R, DV, HG, KF, CH>;
     const int kgrp = lane / S::LPT, kpart = lane % S::LPT;
     const int vgrp = lane / S::LPV;
     c.nvalid = nvalid;
@@ -177,24 +201,39 @@ __device__ __forceinline__ void process_chunk(Chunk<R, DV, HG, FP8, CH>& c, int 
     float s[S::KL][HG];
 #pragma unroll
     for (int j = 0; j < S::KL; ++j) {
-        const uint32_t w[4] = {c.k[j].x, c.k[j].y, c.k[j].z, c.k[j].w};
         uint32_t kb[S::QW];  // key slice as packed bf16 pairs
+        if constexpr (KF == kKeyInt4) {
+            // nibble n -> bf16 128 + n (exponent byte 0x43, n in the low mantissa
+            // bits), pairs (entry 2m, entry 2m + 1); the excess 136 = 128 + 8 per
+            // entry is taken off with the query slice sum below
+            const uint32_t w[2] = {c.k[j].x, c.k[j].y};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if constexpr (FP8) {
-                kb[2 * i] = e4m3x2_bf16<false>(w[i]);
-                kb[2 * i + 1] = e4m3x2_bf16<true>(w[i]);
-            } else {
-                kb[i] = w[i];
+            for (int i = 0; i < 2; ++i) {
+                const uint32_t lo = w[i] & 0x0f0f0f0fu, hi = (w[i] >> 4) & 0x0f0f0f0fu;
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+                    kb[4 * i + m] = __builtin_amdgcn_perm(hi, lo, 0x0c040c00u + 0x00010001u * m) | 0x43004300u;
+            }
+        } else {
+            const uint32_t w[4] = {c.k[j].x, c.k[j].y, c.k[j].z, c.k[j].w};
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if constexpr (KF == kKeyE4M3) {
+                    kb[2 * i] = e4m3x2_bf16<false>(w[i]);
+                    kb[2 * i + 1] = e4m3x2_bf16<true>(w[i]);
+                } else {
+                    kb[i] = w[i];
+                }
             }
         }
         const bool valid = j * S::TPK + kgrp < c.nvalid;
-        const float sc = FP8 ? qscale * c.ks[FP8 ? j : 0] : qscale;
+        const float sc = KeyRow<KF>::SCALED ? qscale * c.ks[KeyRow<KF>::SCALED ? j : 0] : qscale;
 #pragma unroll
         for (int h = 0; h < HG; ++h) {
             float acc = 0.f;
 #pragma unroll
             for (int i = 0; i < S::QW; ++i) acc = dot2_bf16(kb[i], qp[h][i], acc);
+            if constexpr (KF == kKeyInt4) acc = fmaf(-136.f, qsum[h], acc);
             acc = group_sum<S::LPT>(acc);
             s[j][h] = valid ? acc * sc : -INFINITY;
         }
@@ -259,11 +298,11 @@ __device__ __forceinline__ void process_chunk(Chunk<R, DV, HG, FP8, CH>& c, int 
     wave_lds_sync();
 }
 
-template <int R, int DV, int HG, bool FP8, bool PAGED>
+template <int R, int DV, int HG, int KF, bool PAGED>
 __global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split_kernel(const DecodeParams p) {
-    constexpr int CH = DecodeSchedule<R, DV, HG, FP8>::CH;
-    constexpr bool PIPE = DecodeSchedule<R, DV, HG, FP8>::PIPE;
-    using S = DecodeShape<R, DV, HG, FP8, CH>;
+    constexpr int CH = DecodeSchedule<R, DV, HG, KF>::CH;
+    constexpr bool PIPE = DecodeSchedule<R, DV, HG, KF>::PIPE;
+    using S = DecodeShape<R, DV, HG, KF, CH>;
     constexpr int LPV = S::LPV;
 
     __shared__ uint32_t p_lds[kDecodeWaves][CH * HG / 2];
@@ -300,6 +339,16 @@ __global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split
             qp[h][4 * i + 3] = w.w;
         }
     }
+    // 4-bit keys: sum of this lane's query slice per head
+    float qsum[HG];
+#pragma unroll
+    for (int h = 0; h < HG; ++h) {
+        qsum[h] = 0.f;
+        if constexpr (KF == kKeyInt4) {
+#pragma unroll
+            for (int i = 0; i < S::QW; ++i) qsum[h] += bf16lo(qp[h][i]) + bf16hi(qp[h][i]);
+        }
+    }
 
     WaveState<HG> st;
 #pragma unroll
@@ -323,25 +372,25 @@ __global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split
     first_avail = first_avail < p.max_ctx ? first_avail : p.max_ctx;
     if (PAGED) first_avail = split_end;
     if (ts < first_avail) {
-        using C = Chunk<R, DV, HG, FP8, CH>;
+        using C = Chunk<R, DV, HG, KF, CH>;
         if constexpr (PIPE) {
             C ca, cb;
-            bool ok_a = load_chunk<R, DV, HG, FP8, CH, PAGED>(ca, p, b, g, ts, first_avail, lane), ok_b = true;
+            bool ok_a = load_chunk<R, DV, HG, KF, CH, PAGED>(ca, p, b, g, ts, first_avail, lane), ok_b = true;
             while (true) {
                 const bool more_b = ts + kStride < split_end;
-                if (more_b) ok_b = load_chunk<R, DV, HG, FP8, CH, PAGED>(cb, p, b, g, ts + kStride, split_end, lane);
+                if (more_b) ok_b = load_chunk<R, DV, HG, KF, CH, PAGED>(cb, p, b, g, ts + kStride, split_end, lane);
                 if (ts < split_end) {
                     bad_block |= !ok_a;
-                    if (ok_a) process_chunk<R, DV, HG, FP8, CH>(ca, split_end - ts < CH ? split_end - ts : CH, st, qp,
-                                                                p.qscale, p16, lane);
+                    if (ok_a) process_chunk<R, DV, HG, KF, CH>(ca, split_end - ts < CH ? split_end - ts : CH, st, qp,
+                                                                qsum, p.qscale, p16, lane);
                 }
                 if (!more_b) break;
                 ts += kStride;
                 const bool more_a = ts + kStride < split_end;
-                if (more_a) ok_a = load_chunk<R, DV, HG, FP8, CH, PAGED>(ca, p, b, g, ts + kStride, split_end, lane);
+                if (more_a) ok_a = load_chunk<R, DV, HG, KF, CH, PAGED>(ca, p, b, g, ts + kStride, split_end, lane);
                 bad_block |= !ok_b;
-                if (ok_b) process_chunk<R, DV, HG, FP8, CH>(cb, split_end - ts < CH ? split_end - ts : CH, st, qp,
-                                                            p.qscale, p16, lane);
+                if (ok_b) process_chunk<R, DV, HG, KF, CH>(cb, split_end - ts < CH ? split_end - ts : CH, st, qp,
+                                                            qsum, p.qscale, p16, lane);
                 if (!more_a) break;
                 ts += kStride;
             }
@@ -349,11 +398,11 @@ __global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split
             int avail = first_avail;
             for (; ts < avail; ts += kStride, avail = split_end) {
                 C ca;
-                const bool ok = load_chunk<R, DV, HG, FP8, CH, PAGED>(ca, p, b, g, ts, avail, lane);
+                const bool ok = load_chunk<R, DV, HG, KF, CH, PAGED>(ca, p, b, g, ts, avail, lane);
                 if (ts >= split_end) break;
                 bad_block |= !ok;
-                if (ok) process_chunk<R, DV, HG, FP8, CH>(ca, split_end - ts < CH ? split_end - ts : CH, st, qp,
-                                                          p.qscale, p16, lane);
+                if (ok) process_chunk<R, DV, HG, KF, CH>(ca, split_end - ts < CH ? split_end - ts : CH, st, qp,
+                                                          qsum, p.qscale, p16, lane);
             }
         }
     }
@@ -510,44 +559,53 @@ DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV) {
 
 // ------------------------------------------------------------------ dispatch
 
-template <int R, int DV, int HG, bool FP8, bool PAGED>
+template <int R, int DV, int HG, int KF, bool PAGED>
 static hipError_t run(const DecodeParams& p, hipStream_t st) {
     dim3 grid(p.n_split, p.Hkv * (p.G / HG), p.B);
-    hipLaunchKernelGGL((decode_split_kernel<R, DV, HG, FP8, PAGED>), grid, dim3(kDecodeThreads), 0, st, p);
+    hipLaunchKernelGGL((decode_split_kernel<R, DV, HG, KF, PAGED>), grid, dim3(kDecodeThreads), 0, st, p);
     return hipGetLastError();
 }
 
+template <int R, int DV, int HG, int KF>
+static hipError_t by_paging(const DecodeParams& p, bool paged, hipStream_t st) {
+    return paged ? run<R, DV, HG, KF, true>(p, st) : run<R, DV, HG, KF, false>(p, st);
+}
+
 template <int R, int DV, int HG>
-static hipError_t by_layout(const DecodeParams& p, bool fp8, bool paged, hipStream_t st) {
-    if (fp8) return paged ? run<R, DV, HG, true, true>(p, st) : run<R, DV, HG, true, false>(p, st);
-    return paged ? run<R, DV, HG, false, true>(p, st) : run<R, DV, HG, false, false>(p, st);
+static hipError_t by_layout(const DecodeParams& p, int kf, bool paged, hipStream_t st) {
+    switch (kf) {
+        case kKeyBF16: return by_paging<R, DV, HG, kKeyBF16>(p, paged, st);
+        case kKeyE4M3: return by_paging<R, DV, HG, kKeyE4M3>(p, paged, st);
+        case kKeyInt4: return by_paging<R, DV, HG, kKeyInt4>(p, paged, st);
+        default: return hipErrorInvalidValue;
+    }
 }
 
 template <int R, int DV>
-static hipError_t by_group(const DecodeParams& p, int HG, bool fp8, bool paged, hipStream_t st) {
+static hipError_t by_group(const DecodeParams& p, int HG, int kf, bool paged, hipStream_t st) {
     switch (HG) {
-        case 1: return by_layout<R, DV, 1>(p, fp8, paged, st);
-        case 2: return by_layout<R, DV, 2>(p, fp8, paged, st);
-        case 4: return by_layout<R, DV, 4>(p, fp8, paged, st);
-        case 8: return by_layout<R, DV, 8>(p, fp8, paged, st);
+        case 1: return by_layout<R, DV, 1>(p, kf, paged, st);
+        case 2: return by_layout<R, DV, 2>(p, kf, paged, st);
+        case 4: return by_layout<R, DV, 4>(p, kf, paged, st);
+        case 8: return by_layout<R, DV, 8>(p, kf, paged, st);
         default: return hipErrorInvalidValue;
     }
 }
 
 template <int R>
-static hipError_t by_dv(const DecodeParams& p, int DV, int HG, bool fp8, bool paged, hipStream_t st) {
-    if (DV == 64) return by_group<R, 64>(p, HG, fp8, paged, st);
-    if (DV == 128) return by_group<R, 128>(p, HG, fp8, paged, st);
+static hipError_t by_dv(const DecodeParams& p, int DV, int HG, int kf, bool paged, hipStream_t st) {
+    if (DV == 64) return by_group<R, 64>(p, HG, kf, paged, st);
+    if (DV == 128) return by_group<R, 128>(p, HG, kf, paged, st);
     return hipErrorInvalidValue;
 }
 
-tk_status launch_decode(const DecodeParams& p, int R, int DV, int HG, bool fp8, bool paged, hipStream_t st) {
+tk_status launch_decode(const DecodeParams& p, int R, int DV, int HG, int key_format, bool paged, hipStream_t st) {
     hipError_t e;
     switch (R) {
-        case 16: e = by_dv<16>(p, DV, HG, fp8, paged, st); break;
-        case 32: e = by_dv<32>(p, DV, HG, fp8, paged, st); break;
-        case 64: e = by_dv<64>(p, DV, HG, fp8, paged, st); break;
-        case 128: e = by_dv<128>(p, DV, HG, fp8, paged, st); break;
+        case 16: e = by_dv<16>(p, DV, HG, key_format, paged, st); break;
+        case 32: e = by_dv<32>(p, DV, HG, key_format, paged, st); break;
+        case 64: e = by_dv<64>(p, DV, HG, key_format, paged, st); break;
+        case 128: e = by_dv<128>(p, DV, HG, key_format, paged, st); break;
         default: return TK_ERR_UNSUPPORTED;
     }
     if (e == hipErrorInvalidValue) return TK_ERR_UNSUPPORTED;

@@ -11,10 +11,15 @@ namespace tk {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// Key formats of the cache: bf16 rows, OCP E4M3 codes, or 4-bit integer codes
+// (excess-8 nibbles, two per byte, low nibble first); the quantised formats
+// carry one fp32 scale per (token, KV head).
+enum KeyFormat : int { kKeyBF16 = 0, kKeyE4M3 = 1, kKeyInt4 = 2 };
+
 // Decode: one 256-thread workgroup per (split, KV head x head group, sequence).
 struct DecodeParams {
     const uint16_t* q;          // [B, Hq, R] bf16
-    const uint8_t* k;           // key rows: bf16 (2R bytes) or E4M3 codes (R bytes)
+    const uint8_t* k;           // key rows: bf16 (2R bytes), E4M3 codes (R bytes) or 4-bit codes (R/2 bytes)
     const float* k_scale;       // per key row (fp8 only)
     const uint16_t* v;          // value rows, DV bf16
     const int32_t* ctx_lens;    // [B]
@@ -39,7 +44,7 @@ struct DecodePlan {
 // Pure function of the shapes (no device query).
 DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV);
 
-tk_status launch_decode(const DecodeParams& p, int R, int DV, int HG, bool fp8, bool paged,
+tk_status launch_decode(const DecodeParams& p, int R, int DV, int HG, int key_format, bool paged,
                         hipStream_t stream);
 
 // Cache append: grid-stride over 16-byte row slices of the new tokens.
@@ -47,8 +52,8 @@ struct AppendParams {
     const uint16_t* kn;         // [B, Hkv, T, R] bf16 new key rows
     const uint16_t* vn;         // [B, Hkv, T, DV] bf16 new value rows
     const int32_t* pos;         // [B] first position written
-    uint8_t* kc;                // key cache rows: bf16 (2R bytes) or E4M3 codes (R bytes)
-    float* ks;                  // per key row scale (fp8 only)
+    uint8_t* kc;                // key cache rows: bf16 (2R bytes), E4M3 codes (R bytes) or 4-bit codes (R/2)
+    float* ks;                  // per key row scale (quantised keys only)
     uint16_t* vc;               // value cache rows
     const int32_t* table;       // [B, mb] or null
     int B, Hkv, T;
@@ -56,7 +61,7 @@ struct AppendParams {
     int bs_log2, mb, num_blocks;
 };
 
-tk_status launch_append(const AppendParams& p, int R, int DV, bool fp8, bool paged, hipStream_t stream);
+tk_status launch_append(const AppendParams& p, int R, int DV, int key_format, bool paged, hipStream_t stream);
 
 struct PrefillParams {
     const void* q;   // [B, Hq, Sq, R]

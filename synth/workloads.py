@@ -63,7 +63,7 @@ class DecodeSpec:
     ctx: int                     # max context (sizes the contiguous cache)
     r: int
     d_v: int
-    k_dtype: str = "bf16"        # "bf16" or "fp8"
+    k_dtype: str = "bf16"        # "bf16", "fp8" (E4M3) or "int4"
     paged: bool = False
     block_size: int = 256
     ctx_lens: Optional[Tuple[int, ...]] = None  # ragged lengths; None -> all ctx
@@ -99,15 +99,23 @@ WORKLOADS = {
     "fp8key_decode": DecodeSpec("fp8key_decode", 5, 32, 32, 8, 32768, 32, 128, k_dtype="fp8"),
 }
 
+# Thin keys composed with 4-bit quantisation (the composition the discussion in
+# Sec. 6 proposes): the fp8-key workload with 4-bit integer keys.
+INT4KEY = {"int4key_decode": DecodeSpec("int4key_decode", 5, 32, 32, 8, 32768, 32, 128, k_dtype="int4")}
+
 
 # Full-key controls: the same workloads with standard-width keys (r = d_head =
 # 128, scale 1/sqrt(128)) and the same value streams, so that thin-key and
 # full-key attention can be timed side by side (the decode saving the paper
 # predicts from the byte ratio, Eq. 8-10, and the prefill selection cost).
+# The 4-bit-key decode's control has standard-width bf16 keys: it measures the
+# composition of thin keys with 4-bit quantisation (Sec. 6) against plain keys.
 FULLKEY = {
     name + "_fullkey": replace(WORKLOADS[name], name=name + "_fullkey", r=128)
     for name in ("mistral_decode_b16", "mistral_prefill_s8192", "longctx_paged_decode")
 }
+FULLKEY["int4key_decode_fullkey"] = replace(INT4KEY["int4key_decode"], name="int4key_decode_fullkey", r=128,
+                                            k_dtype="bf16")
 
 
 def _draw(spec_id: int, tensor: int, shape, device, amp: float = 1.0) -> torch.Tensor:
@@ -129,6 +137,21 @@ def quantize_e4m3(k: torch.Tensor):
     scale = torch.where(amax > 0, amax / E4M3_MAX, torch.ones_like(amax)).to(torch.float32)
     codes = (k / scale.unsqueeze(-1)).to(torch.float8_e4m3fn).view(torch.uint8)
     return codes, scale
+
+
+INT4_MAX = 7.0
+
+
+def quantize_int4(k: torch.Tensor):
+    """Per-row (last axis, even length) 4-bit integer codes and fp32 scales:
+    scale = max|k| / 7 (1 where the row is all zero), code = k / scale rounded
+    half-to-even and clipped to [-7, 7], stored excess-8 two per byte (entry 2j in
+    the low nibble of byte j). Returns (packed uint8 [..., r / 2], scales fp32 [...])."""
+    k = k.to(torch.float32)
+    amax = k.abs().amax(dim=-1)
+    scale = torch.where(amax > 0, amax / INT4_MAX, torch.ones_like(amax)).to(torch.float32)
+    n = torch.round(k / scale.unsqueeze(-1)).clamp(-7, 7).to(torch.int32) + 8
+    return (n[..., 0::2] | (n[..., 1::2] << 4)).to(torch.uint8), scale
 
 
 def make_prefill(spec: PrefillSpec, device="cpu", structured: bool = False):
@@ -196,6 +219,8 @@ def make_decode(spec: DecodeSpec, device="cpu", structured: bool = False):
     q = q.to(torch.bfloat16)
     if spec.k_dtype == "fp8":
         k, k_scale = quantize_e4m3(kf)
+    elif spec.k_dtype == "int4":
+        k, k_scale = quantize_int4(kf)
     else:
         k, k_scale = kf.to(torch.bfloat16), None
     del kf

@@ -2,7 +2,7 @@
 binding, oracle references and the error gates.
 
 Gates (max-abs against the fp64 oracle on the same inputs): 1e-4 for fp32
-outputs, 2e-2 for bf16 outputs, 5e-2 with fp8 keys. Because i.i.d. inputs give
+outputs, 2e-2 for bf16 outputs, 5e-2 with fp8 or 4-bit keys. Because i.i.d. inputs give
 near-uniform attention and small outputs, a relative L2 gate is applied too
 (1e-5 fp32, 1e-2 otherwise), and the structured inputs make outputs O(1)."""
 from __future__ import annotations
@@ -14,7 +14,7 @@ import torch
 
 from oracle import oracle as orc
 
-TOL = {"f32": (1e-4, 1e-5), "bf16": (2e-2, 1e-2), "fp8": (5e-2, 1e-2)}
+TOL = {"f32": (1e-4, 1e-5), "bf16": (2e-2, 1e-2), "fp8": (5e-2, 1e-2), "int4": (5e-2, 1e-2)}
 
 
 def device():
@@ -60,7 +60,10 @@ def decode_oracle(d, spec, batches=None):
         idx = torch.tensor(batches)
         q, k, v, lens = q[idx], k[idx], v[idx], lens.cpu()[idx]
         ks = None if ks is None else ks[idx]
-    return orc.decode(q.cpu(), k.cpu(), v.cpu(), lens.cpu(), scale=spec.softmax_scale,
+    k = k.cpu()
+    if getattr(spec, "k_dtype", "bf16") == "int4":
+        k = orc.Int4(k)
+    return orc.decode(q.cpu(), k, v.cpu(), lens.cpu(), scale=spec.softmax_scale,
                       k_scale=None if ks is None else ks.cpu())
 
 

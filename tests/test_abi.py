@@ -75,6 +75,7 @@ def decode(**kw):
     (dict(max_ctx=-1), tb.TK_ERR_INVALID_ARG),
     (dict(k_dtype=tb.TK_FP8_E4M3), tb.TK_ERR_INVALID_ARG),     # fp8 without scales
     (dict(k_scale=P), tb.TK_ERR_INVALID_ARG),                  # scales without fp8
+    (dict(k_dtype=tb.TK_INT4), tb.TK_ERR_INVALID_ARG),         # 4-bit keys without scales
     (dict(k_dtype=tb.TK_F32), tb.TK_ERR_UNSUPPORTED),
     (dict(block_size=256), tb.TK_ERR_INVALID_ARG),             # layout args without a table
     (dict(block_table=P, block_size=0, max_blocks=16, num_blocks=32), tb.TK_ERR_INVALID_ARG),
@@ -119,6 +120,7 @@ def append(**kw):
     (dict(max_ctx=-1), tb.TK_ERR_INVALID_ARG),
     (dict(k_dtype=tb.TK_FP8_E4M3), tb.TK_ERR_INVALID_ARG),     # fp8 without scales
     (dict(k_scale=P), tb.TK_ERR_INVALID_ARG),                  # scales without fp8
+    (dict(k_dtype=tb.TK_INT4), tb.TK_ERR_INVALID_ARG),         # 4-bit keys without scales
     (dict(k_dtype=tb.TK_F32), tb.TK_ERR_UNSUPPORTED),
     (dict(block_size=64), tb.TK_ERR_INVALID_ARG),              # layout args without a table
     (dict(block_table=P, block_size=0, max_blocks=4, num_blocks=8), tb.TK_ERR_INVALID_ARG),

@@ -30,7 +30,8 @@ def fill_bytes(shape, key, dtype):
     return x.to(dtype)
 
 
-def run(B, Hkv, T, r, dv, fp8, paged, positions, bs=16, mb=None, key=0, bad=None):
+def run(B, Hkv, T, r, dv, kdt, paged, positions, bs=16, mb=None, key=0, bad=None):
+    """kdt: "bf16", "fp8" (True) or "int4" key cache."""
     from paper_2603_04427_amd import tk_cache_append
     dev = device()
     k = bf16((B, Hkv, T, r), 100 + key, amp=2.0)
@@ -47,13 +48,18 @@ def run(B, Hkv, T, r, dv, fp8, paged, positions, bs=16, mb=None, key=0, bad=None
         table = None
         cap = mb or 64
         shape_k, shape_v = (B, Hkv, cap, r), (B, Hkv, cap, dv)
+    kdt = {True: "fp8", False: "bf16"}.get(kdt, kdt)
+    fp8 = kdt != "bf16"
+    if kdt == "int4":
+        shape_k = (*shape_k[:3], r // 2)
     kc = fill_bytes(shape_k, 400 + key, torch.uint8 if fp8 else torch.bfloat16)
     vc = fill_bytes(shape_v, 500 + key, torch.bfloat16)
     ks = normal(stream_key(600 + key, 1), math.prod(shape_k[:3])).view(*shape_k[:3]).abs() if fp8 else None
-    ref = oa.cache_append(k, v, pos, kc, vc, k_scale=ks, block_table=table, block_size=bs if paged else 0)
+    ref = oa.cache_append(k, v, pos, kc, vc, k_scale=ks, block_table=table, block_size=bs if paged else 0,
+                          k_format=kdt)
     gk, gv = kc.to(dev), vc.to(dev)
     gs = None if ks is None else ks.to(dev)
-    say(f"append B={B} Hkv={Hkv} T={T} r={r} dv={dv} fp8={fp8} paged={paged} pos={positions}")
+    say(f"append B={B} Hkv={Hkv} T={T} r={r} dv={dv} keys={kdt} paged={paged} pos={positions}")
     tk_cache_append(k.to(dev), v.to(dev), pos.to(dev), gk, gv, k_scale=gs,
                     block_table=None if table is None else table.to(dev), block_size=bs if paged else 0)
     torch.cuda.synchronize()
@@ -65,10 +71,10 @@ def run(B, Hkv, T, r, dv, fp8, paged, positions, bs=16, mb=None, key=0, bad=None
 
 @pytest.mark.parametrize("r", [16, 32, 64, 128])
 @pytest.mark.parametrize("dv", [64, 128])
-@pytest.mark.parametrize("fp8", [False, True])
+@pytest.mark.parametrize("kdt", ["bf16", "fp8", "int4"])
 @pytest.mark.parametrize("paged", [False, True])
-def test_sweep_bitexact(r, dv, fp8, paged):
-    run(3, 2, 37, r, dv, fp8, paged, positions=[0, 50, 90], key=r + dv)
+def test_sweep_bitexact(r, dv, kdt, paged):
+    run(3, 2, 37, r, dv, kdt, paged, positions=[0, 50, 90], key=r + dv)
 
 
 @pytest.mark.parametrize("T,positions", [(1, [0, 5, 127]), (1, [-1, 128, 64]), (300, [-7, 0, 100]),
@@ -83,9 +89,9 @@ def test_bad_block_entry_skipped():
 
 
 def test_prefill_scale_append_bitexact():
-    """The 8192-token, 4 x 8 KV-head shape of the prefill workload, bf16 and fp8 keys."""
-    for fp8 in (False, True):
-        run(4, 8, 8192, 32, 128, fp8, False, [0, 0, 0, 0], mb=8192, key=11)
+    """The 8192-token, 4 x 8 KV-head shape of the prefill workload, bf16, fp8 and 4-bit keys."""
+    for kdt in ("bf16", "fp8", "int4"):
+        run(4, 8, 8192, 32, 128, kdt, False, [0, 0, 0, 0], mb=8192, key=11)
 
 
 def test_append_then_decode():
@@ -94,22 +100,24 @@ def test_append_then_decode():
     from paper_2603_04427_amd import tk_attn_decode, tk_cache_append
     dev = device()
     B, Hq, Hkv, r, dv, bs, mb = 3, 8, 2, 32, 128, 64, 8
-    for fp8 in (False, True):
+    for kdt in ("bf16", "fp8", "int4"):
+        fp8 = kdt != "bf16"
         lens = [300, 511, 1]
         T0 = max(lens) - 1
         k0, v0 = bf16((B, Hkv, T0, r), 700, amp=2.0), bf16((B, Hkv, T0, dv), 701)
         k1, v1 = bf16((B, Hkv, 1, r), 702, amp=2.0), bf16((B, Hkv, 1, dv), 703)
         q = bf16((B, Hq, r), 704, amp=2.0)
         table = permutation(stream_key(705, 3), B * mb).view(B, mb).to(torch.int32)
-        kc = torch.zeros(B * mb, Hkv, bs, r, dtype=torch.uint8 if fp8 else torch.bfloat16)
+        kc = torch.zeros(B * mb, Hkv, bs, r // 2 if kdt == "int4" else r,
+                         dtype=torch.uint8 if fp8 else torch.bfloat16)
         vc = torch.zeros(B * mb, Hkv, bs, dv, dtype=torch.bfloat16)
         ks = torch.ones(B * mb, Hkv, bs) if fp8 else None
         pos0 = torch.zeros(B, dtype=torch.int32)
         pos1 = torch.tensor([L - 1 for L in lens], dtype=torch.int32)
-        rk, rv, rs = oa.cache_append(k0, v0, pos0, kc, vc, ks, table, bs)
-        rk, rv, rs = oa.cache_append(k1, v1, pos1, rk, rv, rs, table, bs)
+        rk, rv, rs = oa.cache_append(k0, v0, pos0, kc, vc, ks, table, bs, k_format=kdt)
+        rk, rv, rs = oa.cache_append(k1, v1, pos1, rk, rv, rs, table, bs, k_format=kdt)
         gk, gv, gs, gt = kc.to(dev), vc.to(dev), None if ks is None else ks.to(dev), table.to(dev)
-        say(f"append+decode fp8={fp8}")
+        say(f"append+decode keys={kdt}")
         tk_cache_append(k0.to(dev), v0.to(dev), pos0.to(dev), gk, gv, gs, gt, bs)
         tk_cache_append(k1.to(dev), v1.to(dev), pos1.to(dev), gk, gv, gs, gt, bs)
         lens_t = torch.tensor(lens, dtype=torch.int32)
@@ -121,5 +129,6 @@ def test_append_then_decode():
         logical_v = torch.stack([torch.cat([rv[int(table[b, j])] for j in range(mb)], dim=1) for b in range(B)])
         logical_s = None if rs is None else torch.stack(
             [torch.cat([rs[int(table[b, j])] for j in range(mb)], dim=1) for b in range(B)])
-        ref = orc.decode(q, logical_k, logical_v, lens_t, k_scale=logical_s)
-        gate(out, ref, "fp8" if fp8 else "bf16", f"append+decode fp8={fp8}")
+        ref = orc.decode(q, orc.Int4(logical_k) if kdt == "int4" else logical_k, logical_v, lens_t,
+                         k_scale=logical_s)
+        gate(out, ref, kdt, f"append+decode keys={kdt}")

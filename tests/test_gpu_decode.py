@@ -7,7 +7,7 @@ import pytest
 import torch
 
 from gpu_cases import decode_on_gpu, decode_oracle, device, gate, say
-from synth import FULLKEY, WORKLOADS, DecodeSpec, make_decode, with_shape
+from synth import FULLKEY, INT4KEY, WORKLOADS, DecodeSpec, make_decode, with_shape
 
 pytestmark = pytest.mark.gpu
 
@@ -28,14 +28,14 @@ def run_case(spec, structured=False, batches=None, on_gpu_inputs=False):
 
 @pytest.mark.parametrize("r", [16, 32, 64, 128])
 @pytest.mark.parametrize("dv", [64, 128])
-@pytest.mark.parametrize("fp8", [False, True])
+@pytest.mark.parametrize("kdt", ["bf16", "fp8", "int4"])
 @pytest.mark.parametrize("paged", [False, True])
-def test_sweep_shapes(r, dv, fp8, paged):
-    spec = with_shape(BASE, config_id=100 + r + dv, r=r, d_v=dv, k_dtype="fp8" if fp8 else "bf16",
+def test_sweep_shapes(r, dv, kdt, paged):
+    spec = with_shape(BASE, config_id=100 + r + dv, r=r, d_v=dv, k_dtype=kdt,
                       paged=paged, block_size=64, ctx=320, ctx_lens=(320, 1, 200))
     for structured in (False, True):
         out, ref = run_case(spec, structured)
-        gate(out, ref, "fp8" if fp8 else "bf16", f"{spec} structured={structured}")
+        gate(out, ref, kdt, f"{spec} structured={structured}")
 
 
 @pytest.mark.parametrize("G", [1, 2, 3, 4, 8, 16])
@@ -83,11 +83,13 @@ def test_longctx_paged_decode_full_sampled(name):
     say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
 
 
-def test_fp8key_decode_full_sampled():
-    """Batch 32, context 32768, E4M3 keys with per-token-head scales; oracle on 3 sequences."""
-    spec = WORKLOADS["fp8key_decode"]
+@pytest.mark.parametrize("name", ["fp8key_decode", "int4key_decode", "int4key_decode_fullkey"])
+def test_quantised_key_decode_full_sampled(name):
+    """Batch 32, context 32768, E4M3 or 4-bit keys with per-token-head scales, and the
+    standard-key control of that shape (r 128, bf16); oracle on 3 sequences."""
+    spec = {**WORKLOADS, **INT4KEY, **FULLKEY}[name]
     out, ref = run_case(spec, structured=True, batches=[0, 13, 31], on_gpu_inputs=True)
-    mx, rel = gate(out, ref, "fp8", "fp8key_decode")
+    mx, rel = gate(out, ref, spec.k_dtype, name)
     say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
 
 

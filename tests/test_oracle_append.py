@@ -101,3 +101,32 @@ def test_rounding_matches_brute_force_nearest_even_code():
     for xv, g in zip(x.tolist(), got):
         best = min(table, key=lambda cv: (abs(cv[1] - xv), cv[0] & 1))
         assert g == best[0], (xv, g, best)
+
+
+def test_int4_hand_computed_row():
+    """k = (1, -2, 0.5, 0.15, 0, ...): max|k| = 2 and scale = fp32(2/7), which lies just
+    above 2/7, so in fp32 k/scale = (3.4999998, -6.9999998, 1.7499999, 0.525): the
+    codes are (3, -7, 2, 1), not the 4 an exact 3.5 would give; stored excess-8 as
+    nibbles (11, 1, 10, 9): bytes 0x1B, 0x9A."""
+    k = torch.zeros(1, 16)
+    k[0, :4] = torch.tensor([1.0, -2.0, 0.5, 0.15])
+    packed, scale = oa.quantize_rows_int4(k)
+    assert packed[0, :3].tolist() == [0x1B, 0x9A, 0x88]
+    assert scale.item() == float(torch.tensor(2.0) / torch.tensor(7.0))
+
+
+def test_int4_round_half_even_and_bound():
+    """Ties go to the even integer (2.5 -> 2, 3.5 -> 4, -0.5 -> 0); every decoded entry
+    lies within scale / 2 of the input, and the peak entry codes to +-7."""
+    x = torch.tensor([[7.0, 2.5, 3.5, -0.5, 0.5, -2.5, 6.5, -6.5]])
+    packed, scale = oa.quantize_rows_int4(x)
+    assert scale.item() == 1.0
+    c = [int(orc.int4_value(packed[0], i)) for i in range(8)]
+    assert c == [7, 2, 4, 0, 0, -2, 6, -6]
+    k = (normal(stream_key(12, 0), 64 * 32).view(64, 32) * 3).float()
+    packed, scale = oa.quantize_rows_int4(k)
+    dec = torch.tensor([[orc.int4_value(packed[i], j) for j in range(32)] for i in range(64)], dtype=torch.float64)
+    err = (dec * scale.double().unsqueeze(-1) - k.double()).abs()
+    assert torch.all(err <= scale.double().unsqueeze(-1) / 2 * (1 + 1e-6))
+    peak = k.abs().argmax(dim=-1)
+    assert torch.all(dec.gather(1, peak.unsqueeze(1)).abs() == 7)

@@ -34,6 +34,9 @@ MUTANTS = {
     "e4m3_bias": ("mag = ldexp(1.0 + (double)m / 8.0, e - 7);", "mag = ldexp(1.0 + (double)m / 8.0, e - 8);"),
     "e4m3_subnormal": ("mag = ldexp((double)m / 8.0, -6);", "mag = ldexp((double)m / 8.0, -7);"),
     "max_not_subtracted_uses_first": ("m = s[j] > m ? s[j] : m;", "m = s[0];"),
+    "int4_nibble_order": ("const int n = (i & 1) ? (byte >> 4) : (byte & 15);",
+                          "const int n = (i & 1) ? (byte & 15) : (byte >> 4);"),
+    "int4_excess": ("return (double)(n - 8);", "return (double)(n - 7);"),
     "bf16_widening": ("uint32_t w = (uint32_t)bits << 16;", "uint32_t w = ((uint32_t)bits << 16) | 0x8000u;"),
 }
 

@@ -290,6 +290,30 @@ def test_brute_force_fp8_keys():
     assert (o - torch.tensor(ref, dtype=torch.float64)).abs().max().item() < 1e-13
 
 
+def test_brute_force_int4_keys():
+    """4-bit integer keys (excess-8 nibbles, low nibble first) with per-(token, head)
+    scales; codes and packing written here independently, brute force on c * scale."""
+    import random
+    B, Hq, Hkv, ctx, r, dv = 2, 4, 2, 7, 16, 6
+    rng = random.Random(240)
+    codes = [[[[rng.randint(-7, 7) for _ in range(r)] for _ in range(ctx)] for _ in range(Hkv)] for _ in range(B)]
+    packed = torch.tensor([[[[(row[2 * j] + 8) | ((row[2 * j + 1] + 8) << 4) for j in range(r // 2)]
+                             for row in head] for head in seq] for seq in codes], dtype=torch.uint8)
+    sc = torch.rand(B, Hkv, ctx, generator=torch.Generator().manual_seed(241)).float() + 0.1
+    khat = [[[[c * float(sc[b, g, t]) for c in codes[b][g][t]] for t in range(ctx)] for g in range(Hkv)]
+            for b in range(B)]
+    q, v = rnd(242, B, Hq, r), rnd(243, B, Hkv, ctx, dv)
+    o = orc.decode(q, orc.Int4(packed), v, torch.tensor([7, 3], dtype=torch.int32), scale=0.25, k_scale=sc)
+    ref = brute.decode(nested(q), khat, nested(v), [7, 3], 0.25)
+    assert (o - torch.tensor(ref, dtype=torch.float64)).abs().max().item() < 1e-13
+
+
+def test_int4_decode_every_nibble():
+    for n in range(16):
+        row = torch.tensor([n | ((15 - n) << 4)], dtype=torch.uint8)
+        assert orc.int4_value(row, 0) == n - 8 and orc.int4_value(row, 1) == 7 - n
+
+
 def test_bf16_and_f32_inputs_widen_exactly():
     q, k, v = rnd(230, 1, 2, 11, 16), rnd(231, 1, 2, 11, 16), rnd(232, 1, 2, 11, 32)
     for dt in (torch.bfloat16, torch.float32):

@@ -184,3 +184,5 @@ def test_kernel_work_figures():
     assert acc.causal_pairs(5, 8) == sum(min(8, i + 3 + 1) for i in range(5)) == 4 + 5 + 6 + 7 + 8
     c5 = WORKLOADS["fp8key_decode"]
     assert acc.decode_bytes(c5.lens, 32, 8, 32, 128, "fp8") == 32 * 8 * 32768 * 292 + 32 * 32 * 32 * 2 + 32 * 32 * 256 + 128
+    # 4-bit keys: 16 bytes of codes and a 4-byte scale per key row
+    assert acc.decode_bytes(c5.lens, 32, 8, 32, 128, "int4") == 32 * 8 * 32768 * 276 + 32 * 32 * 32 * 2 + 32 * 32 * 256 + 128
