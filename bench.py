@@ -249,7 +249,7 @@ def main():
         sys.exit(2)
     import torch
     from synth import FULLKEY, INT4KEY, WORKLOADS
-    workloads = {**WORKLOADS, **INT4KEY}
+    workloads = {**WORKLOADS, **INT4KEY, **FULLKEY}
 
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)

@@ -11,7 +11,8 @@
 //    MFMAs) of one query head; the workgroup covers HPW = gcd(G, 4) heads of one
 //    KV group and 4 / HPW row blocks, so each K/V tile in LDS serves every wave.
 //  * 64-key tiles are double-buffered in LDS and filled straight from global
-//    memory (global_load_lds, 16 bytes per lane), K and V both in their memory
+//    memory (global_load_lds, 16 bytes per lane, issued a whole tile ahead and
+//    awaited only before the barrier that publishes the tile), K and V both in their memory
 //    layout with the 16-byte chunks of each row XOR-swizzled so that the
 //    operand reads below are free of bank conflicts.
 //  * Scores are computed transposed, S^T = K Q^T: each lane holds 16 keys of one
@@ -41,7 +42,6 @@ constexpr int kXcds = 8;
 
 __host__ __device__ constexpr int gcd4(int g) { return (g % 4 == 0) ? 4 : (g % 2 == 0 ? 2 : 1); }
 
-typedef __attribute__((address_space(3))) void* lds_ptr;
 typedef short v4s __attribute__((ext_vector_type(4)));
 
 // Row swizzle of a tile with W bf16 per row: the 16-byte chunk c of row r is
@@ -94,6 +94,28 @@ struct TileLanes {
     }
 };
 
+// Global->LDS copy of 16 bytes per lane (global_load_lds_dwordx4: lane i writes
+// LDS bytes lds + 16 i .. + 15 from base + off). It is issued as inline assembly
+// on purpose: for the compiler's own form of this copy, every later transposing
+// LDS read waits for all copies in flight, including the next tile's copy into
+// the other buffer, which would stall each tile halfway. The copies are awaited
+// explicitly (wait_loads) before the barrier that publishes a tile. M0, which
+// holds the LDS destination, is restored afterwards.
+__device__ __forceinline__ void copy16_to_lds(const char* base, uint32_t off, const uint16_t* lds) {
+    const uint32_t la = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds;
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %2\n\t"
+        "s_nop 0\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(off), "s"(base), "s"(la)
+        : "memory");
+}
+
 // Issue the copies of the tile starting at key `base` (wave `wave` copies its
 // 1 KB slices). A full tile needs no vector arithmetic: the global base and the
 // LDS destination are wave-uniform and the lane offsets are precomputed. Rows
@@ -110,14 +132,12 @@ __device__ __forceinline__ void load_tile(const TileLanes<R, DV, NT>& tl, uint16
 #pragma unroll
         for (int i = 0; i < T::KL; ++i) {
             if (T::KC % NT != 0 && wave_base + i * NT >= T::KC) break;
-            __builtin_amdgcn_global_load_lds((const void*)(kt + tl.k_off[i]), (lds_ptr)(ks + (wave_base + i * NT) * 8),
-                                             16, 0, 0);
+            copy16_to_lds(kt, tl.k_off[i], ks + (wave_base + i * NT) * 8);
         }
 #pragma unroll
         for (int i = 0; i < T::VL; ++i) {
             if (T::VC % NT != 0 && wave_base + i * NT >= T::VC) break;
-            __builtin_amdgcn_global_load_lds((const void*)(vt + tl.v_off[i]), (lds_ptr)(vs + (wave_base + i * NT) * 8),
-                                             16, 0, 0);
+            copy16_to_lds(vt, tl.v_off[i], vs + (wave_base + i * NT) * 8);
         }
         return;
     }
@@ -126,16 +146,17 @@ __device__ __forceinline__ void load_tile(const TileLanes<R, DV, NT>& tl, uint16
     for (int i = 0; i < T::KL; ++i) {
         if (T::KC % NT != 0 && wave_base + i * NT >= T::KC) break;
         const uint32_t off = (int)tl.k_row[i] > last ? tl.k_off[i] - (tl.k_row[i] - last) * R * 2 : tl.k_off[i];
-        __builtin_amdgcn_global_load_lds((const void*)(kt + off), (lds_ptr)(ks + (wave_base + i * NT) * 8), 16, 0, 0);
+        copy16_to_lds(kt, off, ks + (wave_base + i * NT) * 8);
     }
 #pragma unroll
     for (int i = 0; i < T::VL; ++i) {
         if (T::VC % NT != 0 && wave_base + i * NT >= T::VC) break;
         const uint32_t off = (int)tl.v_row[i] > last ? tl.v_off[i] - (tl.v_row[i] - last) * DV * 2 : tl.v_off[i];
-        __builtin_amdgcn_global_load_lds((const void*)(vt + off), (lds_ptr)(vs + (wave_base + i * NT) * 8), 16, 0, 0);
+        copy16_to_lds(vt, off, vs + (wave_base + i * NT) * 8);
     }
 }
 
+// All of this wave's vector memory operations (the tile copies) have completed.
 __device__ __forceinline__ void wait_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // exp2(s * c - m) for the 16 keys of k-step q of one 32-query block (accumulator
@@ -276,6 +297,10 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_ke
         }
     }
     wait_loads();
+    // the same wait as a builtin, so that the compiler knows the query loads
+    // have landed and adds no wait of its own inside the tile loop (vmcnt 0;
+    // expcnt and lgkmcnt at their maxima)
+    __builtin_amdgcn_s_waitcnt(0x0F70);
     __syncthreads();
 
     for (int t = 0; t < ntiles; ++t) {
