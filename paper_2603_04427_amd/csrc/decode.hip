@@ -35,7 +35,7 @@
 namespace tk {
 
 #ifndef TK_DECODE_WAVES
-#define TK_DECODE_WAVES 8
+#define TK_DECODE_WAVES 4
 #endif
 constexpr int kDecodeWaves = TK_DECODE_WAVES;  // waves per workgroup, each streaming its own chunks
 constexpr int kDecodeThreads = 64 * kDecodeWaves;
@@ -173,32 +173,50 @@ __device__ __forceinline__ bool load_chunk(Chunk<R, DV, HG, KF, CH>& c, const De
     return true;
 }
 
-// Online-softmax state of one wave: running maximum m (log2 domain, the same
-// in every lane), this lane's share of the normaliser l, and its output columns.
-template <int HG>
-struct WaveState {
-    float m[HG], l[HG], o[HG][8];
+// Online-softmax state of one lane. After the row sums every lane of a key row
+// holds the scores of all HG heads; lane kpart (= lane % LPT) keeps heads
+// kpart, kpart + LPT, ... (NH of them), so each score is exponentiated once,
+// without divergent branches. m and l are the reference maximum (log2 domain)
+// and this lane's share of the normaliser of those heads; o holds this lane's
+// output columns of every head, summed over the tokens this lane's row group saw.
+template <int HG, int NH>
+struct LaneState {
+    float m[NH], l[NH], o[HG][8];
 };
 
-// Folds one chunk into the wave's state; rows t >= nvalid of the chunk are
+template <int R, int DV, int HG, int KF, int CH>
+struct LaneHeads {
+    static constexpr int LPT = DecodeShape<R, DV, HG, KF, CH>::LPT;
+    static constexpr int NH = (HG + LPT - 1) / LPT;
+};
+
+// The reference maximum of a head moves only when a score exceeds it by more
+// than kLazy (log2 units), so probabilities stay below 2^kLazy and most chunks
+// need no cross-lane maximum at all. Any reference at or above the true
+// maximum minus kLazy gives the same softmax (the shift cancels in O / l).
+constexpr float kLazy = 8.f;
+
+// Folds one chunk into the lane's state; rows t >= nvalid of the chunk are
 // outside the context (their scores become -inf and their values zero, since
 // cache memory past the context may hold anything).
 template <int R, int DV, int HG, int KF, int CH>
-__device__ __forceinline__ void process_chunk(Chunk<R, DV, HG, KF, CH>& c, int nvalid, WaveState<HG>& st,
+__device__ __forceinline__ void process_chunk(Chunk<R, DV, HG, KF, CH>& c, int nvalid,
+                                              LaneState<HG, LaneHeads<R, DV, HG, KF, CH>::NH>& st,
                                               const uint32_t (&qp)[HG][DecodeShape<R, DV, HG, KF, CH>::QW],
                                               const float (&qsum)[HG], float qscale, uint16_t* p16, int lane) {
     using S = DecodeShape<R, DV, HG, KF, CH>;
-    const int kgrp = lane / S::LPT, kpart = lane % S::LPT;
+    constexpr int LPT = S::LPT;
+    constexpr int NH = LaneHeads<R, DV, HG, KF, CH>::NH;
+    const int kgrp = lane / LPT, kpart = lane % LPT;
     const int vgrp = lane / S::LPV;
-    c.nvalid = nvalid;
     if (nvalid < CH) {  // wave-uniform: only the last chunk of a context
 #pragma unroll
         for (int j = 0; j < S::VL; ++j)
             if (j * S::TPV + vgrp >= nvalid) c.v[j] = make_uint4(0, 0, 0, 0);
     }
 
-    // ---- scores (log2 domain) of this lane's key rows for all HG heads
-    float s[S::KL][HG];
+    // ---- scores (log2 domain) of this lane's key rows, for the lane's own heads
+    float sv[S::KL][NH];
 #pragma unroll
     for (int j = 0; j < S::KL; ++j) {
         uint32_t kb[S::QW];  // key slice as packed bf16 pairs
@@ -226,49 +244,75 @@ __device__ __forceinline__ void process_chunk(Chunk<R, DV, HG, KF, CH>& c, int n
                 }
             }
         }
-        const bool valid = j * S::TPK + kgrp < c.nvalid;
+        const bool valid = j * S::TPK + kgrp < nvalid;
         const float sc = KeyRow<KF>::SCALED ? qscale * c.ks[KeyRow<KF>::SCALED ? j : 0] : qscale;
+        float acc[HG];
 #pragma unroll
         for (int h = 0; h < HG; ++h) {
-            float acc = 0.f;
+            float a = 0.f;
 #pragma unroll
-            for (int i = 0; i < S::QW; ++i) acc = dot2_bf16(kb[i], qp[h][i], acc);
-            if constexpr (KF == kKeyInt4) acc = fmaf(-136.f, qsum[h], acc);
-            acc = group_sum<S::LPT>(acc);
-            s[j][h] = valid ? acc * sc : -INFINITY;
+            for (int i = 0; i < S::QW; ++i) a = dot2_bf16(kb[i], qp[h][i], a);
+            if constexpr (KF == kKeyInt4) a = fmaf(-136.f, qsum[h], a);
+            acc[h] = group_sum<LPT>(a);
+        }
+#pragma unroll
+        for (int i = 0; i < NH; ++i) {
+            float v = acc[i * LPT];
+#pragma unroll
+            for (int t = 1; t < LPT; ++t)
+                if (i * LPT + t < HG) v = kpart == t ? acc[i * LPT + t] : v;
+            if (HG % LPT != 0 && kpart + i * LPT >= HG) v = -INFINITY;  // lane without a head here
+            sv[j][i] = valid ? v * sc : -INFINITY;
         }
     }
 
-    // ---- chunk maximum per head; rescale the running state when it grows
+    // ---- the lazy reference maximum: a wave reduction only when some score
+    // exceeds its head's reference by more than kLazy (always on the first chunk)
+    bool grow = false;
 #pragma unroll
-    for (int h = 0; h < HG; ++h) {
-        float cm = s[0][h];
+    for (int i = 0; i < NH; ++i)
 #pragma unroll
-        for (int j = 1; j < S::KL; ++j) cm = fmaxf(cm, s[j][h]);
-        cm = strided_max<S::LPT>(cm);
-        if (cm > st.m[h]) {  // wave-uniform
-            const float alpha = exp2_fast(st.m[h] - cm);
-            st.m[h] = cm;
-            st.l[h] *= alpha;
+        for (int j = 0; j < S::KL; ++j) grow |= sv[j][i] > st.m[i] + kLazy;
+    if (__builtin_amdgcn_ballot_w64(grow) != 0) {  // wave-uniform
 #pragma unroll
-            for (int e = 0; e < 8; ++e) st.o[h][e] *= alpha;
+        for (int i = 0; i < NH; ++i) {
+            float cm = sv[0][i];
+#pragma unroll
+            for (int j = 1; j < S::KL; ++j) cm = fmaxf(cm, sv[j][i]);
+            cm = strided_max<LPT>(cm);  // over the lanes that own the same heads
+            const bool up = cm > st.m[i];
+            const float alpha = up ? exp2_fast(st.m[i] - cm) : 1.f;
+            st.m[i] = up ? cm : st.m[i];
+            st.l[i] *= alpha;
+            // every lane holds output columns of every head: take each head's
+            // factor from lane t, which owns head i * LPT + t
+#pragma unroll
+            for (int t = 0; t < LPT; ++t) {
+                const int h = i * LPT + t;
+                if (h < HG) {
+                    const float ah = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(alpha), t));
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) st.o[h][e] *= ah;
+                }
+            }
         }
     }
 
-    // ---- probabilities, rounded to bf16, into the LDS pair table: entry
-    // (pair slot, head) holds the tokens of value loads 2q and 2q+1 that the
-    // same lane will combine
+    // ---- probabilities of the lane's heads, rounded to bf16, into the LDS pair
+    // table: entry (pair slot, head) holds the tokens of value loads 2q and 2q+1
+    // that the same lane will combine
 #pragma unroll
     for (int j = 0; j < S::KL; ++j) {
         const int t = j * S::TPK + kgrp;
         const int jv = t / S::TPV, gv = t % S::TPV;
         const int slot = ((jv >> 1) * S::TPV + gv) * HG;
 #pragma unroll
-        for (int h = 0; h < HG; ++h) {
-            if (h % S::LPT == kpart) {
-                const float pr = exp2_fast(s[j][h] - st.m[h]);
+        for (int i = 0; i < NH; ++i) {
+            const int h = kpart + i * LPT;
+            if (HG % LPT == 0 || h < HG) {
+                const float pr = exp2_fast(sv[j][i] - st.m[i]);
                 const uint32_t pb = pack_bf16(pr, 0.f) & 0xffffu;
-                st.l[h] += __uint_as_float(pb << 16);
+                st.l[i] += __uint_as_float(pb << 16);
                 p16[(slot + h) * 2 + (jv & 1)] = (uint16_t)pb;
             }
         }
@@ -298,17 +342,27 @@ __device__ __forceinline__ void process_chunk(Chunk<R, DV, HG, KF, CH>& c, int n
     wave_lds_sync();
 }
 
+// Two workgroups per CU where the registers allow it; 4-bit keys with eight
+// heads per workgroup (their unpacked query slices are twice as wide) take the
+// whole register file of one.
+template <int HG, int KF>
+constexpr int decode_min_blocks() { return KF == kKeyInt4 && HG == 8 ? 1 : 2; }
+
 template <int R, int DV, int HG, int KF, bool PAGED>
-__global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split_kernel(const DecodeParams p) {
+__global__ __launch_bounds__(kDecodeThreads, (decode_min_blocks<HG, KF>())) void decode_split_kernel(
+    const DecodeParams p) {
     constexpr int CH = DecodeSchedule<R, DV, HG, KF>::CH;
     constexpr bool PIPE = DecodeSchedule<R, DV, HG, KF>::PIPE;
     using S = DecodeShape<R, DV, HG, KF, CH>;
     constexpr int LPV = S::LPV;
+    constexpr int ROWS = 64 / LPV;  // lane row groups of a value load (different tokens, same columns)
+    constexpr int LPT = S::LPT;
+    constexpr int NH = LaneHeads<R, DV, HG, KF, CH>::NH;
 
     __shared__ uint32_t p_lds[kDecodeWaves][CH * HG / 2];
     __shared__ float m_lds[kDecodeWaves][HG];
     __shared__ float l_lds[kDecodeWaves][HG];
-    __shared__ float o_lds[kDecodeWaves][HG][DV];
+    __shared__ float o_lds[kDecodeWaves][HG][ROWS][DV];
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
@@ -317,16 +371,11 @@ __global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split
     const int g = blockIdx.y / groups_per_kv;
     const int h0 = g * p.G + (blockIdx.y % groups_per_kv) * HG;
     const int b = blockIdx.z;
-
-    int L = load_uniform(p.ctx_lens + b);
-    L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
     const int split_begin = split * p.split_len;
-    int split_end = split_begin + p.split_len;
-    split_end = split_end < L ? split_end : L;
 
     // this lane's query slice as packed bf16 pairs (exact; the scale is applied in fp32)
     uint32_t qp[HG][S::QW];
-    const int kpart = lane % S::LPT;
+    const int kpart = lane % LPT;
 #pragma unroll
     for (int h = 0; h < HG; ++h) {
         const uint4* qrow = (const uint4*)(p.q + ((size_t)b * p.Hq + h0 + h) * R + kpart * S::EPL);
@@ -350,32 +399,48 @@ __global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split
         }
     }
 
-    WaveState<HG> st;
+    LaneState<HG, NH> st;
 #pragma unroll
-    for (int h = 0; h < HG; ++h) {
-        st.m[h] = -INFINITY;
-        st.l[h] = 0.f;
+    for (int i = 0; i < NH; ++i) {
+        st.m[i] = -INFINITY;
+        st.l[i] = 0.f;
+    }
+#pragma unroll
+    for (int h = 0; h < HG; ++h)
 #pragma unroll
         for (int e = 0; e < 8; ++e) st.o[h][e] = 0.f;
-    }
     bool bad_block = false;
     uint16_t* p16 = (uint16_t*)p_lds[wave];
 
-    // chunks ts, ts + 4 CH, ... of this wave; with PIPE the next chunk's loads
-    // are issued before the current one is processed. For a contiguous cache
-    // the first chunk is requested before the context length has arrived (rows
-    // up to max_ctx are readable); paged caches wait for it, because table
-    // entries past the context need not be valid.
+    // Chunks ts, ts + kStride, ... of this wave; with PIPE the next chunk's loads
+    // are issued before the current one is processed. For a contiguous cache the
+    // first chunk is requested before the context length is read (rows up to
+    // max_ctx are readable), so the length's round trip overlaps the stream;
+    // paged caches wait for it, because table entries past the context need not
+    // be valid.
+    using C = Chunk<R, DV, HG, KF, CH>;
     constexpr int kStride = kDecodeWaves * CH;
     int ts = split_begin + wave * CH;
     int first_avail = split_begin + p.split_len;
     first_avail = first_avail < p.max_ctx ? first_avail : p.max_ctx;
-    if (PAGED) first_avail = split_end;
+    C ca;
+    bool ok_a = true;
+    if constexpr (!PAGED) {
+        if (ts < first_avail) ok_a = load_chunk<R, DV, HG, KF, CH, PAGED>(ca, p, b, g, ts, first_avail, lane);
+        asm volatile("" ::: "memory");  // keep the length's load behind the chunk's loads
+    }
+    int L = load_uniform(p.ctx_lens + b);
+    L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
+    int split_end = split_begin + p.split_len;
+    split_end = split_end < L ? split_end : L;
+    if constexpr (PAGED) {
+        first_avail = split_end;
+        if (ts < first_avail) ok_a = load_chunk<R, DV, HG, KF, CH, PAGED>(ca, p, b, g, ts, first_avail, lane);
+    }
     if (ts < first_avail) {
-        using C = Chunk<R, DV, HG, KF, CH>;
         if constexpr (PIPE) {
-            C ca, cb;
-            bool ok_a = load_chunk<R, DV, HG, KF, CH, PAGED>(ca, p, b, g, ts, first_avail, lane), ok_b = true;
+            C cb;
+            bool ok_b = true;
             while (true) {
                 const bool more_b = ts + kStride < split_end;
                 if (more_b) ok_b = load_chunk<R, DV, HG, KF, CH, PAGED>(cb, p, b, g, ts + kStride, split_end, lane);
@@ -395,70 +460,42 @@ __global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split
                 ts += kStride;
             }
         } else {
-            int avail = first_avail;
-            for (; ts < avail; ts += kStride, avail = split_end) {
-                C ca;
-                const bool ok = load_chunk<R, DV, HG, KF, CH, PAGED>(ca, p, b, g, ts, avail, lane);
+            while (true) {
+                if (ts < split_end) {
+                    bad_block |= !ok_a;
+                    if (ok_a) process_chunk<R, DV, HG, KF, CH>(ca, split_end - ts < CH ? split_end - ts : CH, st, qp,
+                                                                qsum, p.qscale, p16, lane);
+                }
+                ts += kStride;
                 if (ts >= split_end) break;
-                bad_block |= !ok;
-                if (ok) process_chunk<R, DV, HG, KF, CH>(ca, split_end - ts < CH ? split_end - ts : CH, st, qp,
-                                                          qsum, p.qscale, p16, lane);
+                ok_a = load_chunk<R, DV, HG, KF, CH, PAGED>(ca, p, b, g, ts, split_end, lane);
             }
         }
     }
-    float (&m)[HG] = st.m;
-    float (&l)[HG] = st.l;
-    float (&o)[HG][8] = st.o;
 
-    // ---- wave totals: sums over the lanes that saw different rows
+    // ---- this wave's partial into LDS: the raw output sums of every lane row
+    // group (summed over the groups by the merge below), and per head the
+    // reference maximum and the normaliser summed over the lanes owning the head
+    const bool wave_bad = bad_block;  // wave-uniform
 #pragma unroll
     for (int h = 0; h < HG; ++h) {
-        l[h] = strided_sum<1>(l[h]);
-#pragma unroll
-        for (int c = 0; c < 8; ++c) o[h][c] = strided_sum<LPV>(o[h][c]);
+        float* dst = &o_lds[wave][h][lane / LPV][(lane % LPV) * 8];
+        *(float4*)dst = make_float4(st.o[h][0], st.o[h][1], st.o[h][2], st.o[h][3]);
+        *(float4*)(dst + 4) = make_float4(st.o[h][4], st.o[h][5], st.o[h][6], st.o[h][7]);
     }
-    const bool wave_bad = bad_block;  // wave-uniform
-    if (lane < LPV) {
 #pragma unroll
-        for (int h = 0; h < HG; ++h)
-#pragma unroll
-            for (int c = 0; c < 8; ++c) o_lds[wave][h][lane * 8 + c] = o[h][c];
-    }
-    if (lane == 0) {
-#pragma unroll
-        for (int h = 0; h < HG; ++h) {
-            m_lds[wave][h] = m[h];
-            l_lds[wave][h] = wave_bad ? NAN : l[h];
+    for (int i = 0; i < NH; ++i) {
+        const float li = strided_sum<LPT>(st.l[i]);
+        const int h = kpart + i * LPT;
+        if (lane < LPT && h < HG) {
+            m_lds[wave][h] = st.m[i];
+            l_lds[wave][h] = wave_bad ? NAN : li;
         }
     }
     __syncthreads();
 
-    // ---- merge the waves. With a single split that is the answer: normalise and
-    // write the bf16 rows directly.
-    if (p.n_split == 1) {
-        for (int idx = threadIdx.x; idx < HG * DV; idx += kDecodeThreads) {
-            const int h = idx / DV, c = idx % DV;
-            float M = -INFINITY;
-#pragma unroll
-            for (int w = 0; w < kDecodeWaves; ++w) M = fmaxf(M, m_lds[w][h]);
-            float O = 0.f, Lsum = 0.f;
-            bool bad = false;
-#pragma unroll
-            for (int w = 0; w < kDecodeWaves; ++w) {
-                const float mw = m_lds[w][h];
-                const float e = mw == -INFINITY ? 0.f : exp2_fast(mw - M);
-                O = fmaf(e, o_lds[w][h][c], O);
-                Lsum = fmaf(e, l_lds[w][h], Lsum);
-                bad |= __builtin_isnan(l_lds[w][h]);
-            }
-            const float out = bad ? NAN : (M == -INFINITY ? 0.f : O / Lsum);
-            p.o[((size_t)b * p.Hq + h0 + h) * DV + c] = (uint16_t)(pack_bf16(out, 0.f) & 0xffffu);
-        }
-        return;
-    }
-    // Otherwise write this split's partial per head. Partials are written and
-    // read with agent-scope atomic accesses (coherent across the XCDs' separate
-    // L2 caches without an L2 write-back).
+    // ---- merge the waves (log-sum-exp rule). With a single split that is the
+    // answer: normalise and write the bf16 rows directly.
     const int ws_row = DV + 2;
     for (int idx = threadIdx.x; idx < HG * DV; idx += kDecodeThreads) {
         const int h = idx / DV, c = idx % DV;
@@ -466,21 +503,34 @@ __global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split
 #pragma unroll
         for (int w = 0; w < kDecodeWaves; ++w) M = fmaxf(M, m_lds[w][h]);
         float O = 0.f, Lsum = 0.f;
+        bool bad = false;
 #pragma unroll
         for (int w = 0; w < kDecodeWaves; ++w) {
             const float mw = m_lds[w][h];
             const float e = mw == -INFINITY ? 0.f : exp2_fast(mw - M);
-            O = fmaf(e, o_lds[w][h][c], O);
+            float ow = 0.f;
+#pragma unroll
+            for (int r = 0; r < ROWS; ++r) ow += o_lds[w][h][r][c];
+            O = fmaf(e, ow, O);
             Lsum = fmaf(e, l_lds[w][h], Lsum);
-            if (__builtin_isnan(l_lds[w][h])) Lsum = NAN;
+            bad |= __builtin_isnan(l_lds[w][h]);
         }
-        float* dst = p.ws + (((size_t)b * p.Hq + h0 + h) * p.n_split + split) * ws_row;
-        store_coherent(dst + c, O);
-        if (c == 0) {
-            store_coherent(dst + DV, M);
-            store_coherent(dst + DV + 1, Lsum);
+        if (p.n_split == 1) {
+            const float out = bad ? NAN : (M == -INFINITY ? 0.f : O / Lsum);
+            p.o[((size_t)b * p.Hq + h0 + h) * DV + c] = (uint16_t)(pack_bf16(out, 0.f) & 0xffffu);
+        } else {
+            // this split's partial; written and read with agent-scope atomic
+            // accesses (coherent across the XCDs' separate L2 caches without an
+            // L2 write-back)
+            float* dst = p.ws + (((size_t)b * p.Hq + h0 + h) * p.n_split + split) * ws_row;
+            store_coherent(dst + c, O);
+            if (c == 0) {
+                store_coherent(dst + DV, M);
+                store_coherent(dst + DV + 1, bad ? NAN : Lsum);
+            }
         }
     }
+    if (p.n_split == 1) return;
 
     // ---- the last workgroup of this (sequence, head group) to finish merges the
     // splits with the log-sum-exp rule and writes the bf16 output rows
@@ -493,26 +543,28 @@ __global__ __launch_bounds__(kDecodeThreads, 8 / kDecodeWaves) void decode_split
                   (unsigned)(p.n_split - 1);
     __syncthreads();
     if (!is_last) return;
-    // one pass over the splits, 8 at a time (their loads in flight together),
-    // with the running-maximum rule of the online softmax
+    // one pass over the splits, up to 8 at a time (their loads in flight
+    // together), with the running-maximum rule of the online softmax
     for (int idx = threadIdx.x; idx < HG * DV; idx += kDecodeThreads) {
         const int h = idx / DV, c = idx % DV;
         const float* base = p.ws + ((size_t)b * p.Hq + h0 + h) * p.n_split * ws_row;
         float M = -INFINITY, O = 0.f, Lsum = 0.f;
         bool bad = false;
         for (int s0 = 0; s0 < p.n_split; s0 += 8) {
+            const int cnt = p.n_split - s0 < 8 ? p.n_split - s0 : 8;
             float ms[8], ls[8], os[8];
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                const int sp = s0 + i < p.n_split ? s0 + i : p.n_split - 1;
-                const float* part = base + (size_t)sp * ws_row;
-                ms[i] = load_coherent(part + DV);
-                ls[i] = load_coherent(part + DV + 1);
-                os[i] = load_coherent(part + c);
+                if (i < cnt) {
+                    const float* part = base + (size_t)(s0 + i) * ws_row;
+                    ms[i] = load_coherent(part + DV);
+                    ls[i] = load_coherent(part + DV + 1);
+                    os[i] = load_coherent(part + c);
+                }
             }
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
-                if (s0 + i >= p.n_split) break;
+                if (i >= cnt) break;
                 bad |= __builtin_isnan(ls[i]);
                 if (ms[i] == -INFINITY) continue;
                 if (ms[i] > M) {
