@@ -137,6 +137,9 @@ tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache
     p.qscale = resolve_scale(scale, r) * tk::kLog2e;
     // wide keys leave no registers for 8 heads per workgroup: use groups of 4
     const int hg = (r >= 64 && pl.heads_per_group > 4) ? 4 : pl.heads_per_group;
+    // a split context needs one arrival counter per (sequence, head group)
+    if (pl.n_split > 1 && (size_t)batch * H_kv * (H_q / H_kv / hg) * sizeof(unsigned) > pl.counter_bytes)
+        return TK_ERR_UNSUPPORTED;
     return tk::launch_decode(p, r, d_v, hg, key_format(k_dtype), paged, stream);
 }
 

@@ -40,6 +40,8 @@ namespace tk {
 constexpr int kDecodeWaves = TK_DECODE_WAVES;  // waves per workgroup, each streaming its own chunks
 constexpr int kDecodeThreads = 64 * kDecodeWaves;
 constexpr int kMaxSplits = 1024;
+constexpr size_t kCounterRegionBytes = 2 * TK_DECODE_TARGET_GROUPS * sizeof(unsigned);
+static_assert(kCounterRegionBytes % 256 == 0, "the partials after the counters stay 256-byte aligned");
 
 // Agent-scope relaxed atomic accesses (sc1 on gfx950): coherent across XCDs.
 __device__ __forceinline__ void store_coherent(float* p, float v) {
@@ -494,43 +496,66 @@ __global__ __launch_bounds__(kDecodeThreads, (decode_min_blocks<HG, KF>())) void
     }
     __syncthreads();
 
-    // ---- merge the waves (log-sum-exp rule). With a single split that is the
-    // answer: normalise and write the bf16 rows directly.
+    // ---- merge the waves (log-sum-exp rule). Each thread owns kOut output
+    // columns and reads all of their LDS entries before combining them. With a
+    // single split that is the answer: normalise and write the bf16 rows directly.
+    constexpr int kOut = (HG * DV + kDecodeThreads - 1) / kDecodeThreads;
     const int ws_row = DV + 2;
-    for (int idx = threadIdx.x; idx < HG * DV; idx += kDecodeThreads) {
-        const int h = idx / DV, c = idx % DV;
-        float M = -INFINITY;
+    float M[kOut], O[kOut], Lsum[kOut];
+    bool bad[kOut];
 #pragma unroll
-        for (int w = 0; w < kDecodeWaves; ++w) M = fmaxf(M, m_lds[w][h]);
-        float O = 0.f, Lsum = 0.f;
-        bool bad = false;
+    for (int u = 0; u < kOut; ++u) {
+        const int idx = threadIdx.x + u * kDecodeThreads;
+        M[u] = -INFINITY;
+        O[u] = 0.f;
+        Lsum[u] = 0.f;
+        bad[u] = false;
+        if (idx >= HG * DV) continue;
+        const int h = idx / DV, c = idx % DV;
+        float mw[kDecodeWaves], lw[kDecodeWaves], ow[kDecodeWaves];
 #pragma unroll
         for (int w = 0; w < kDecodeWaves; ++w) {
-            const float mw = m_lds[w][h];
-            const float e = mw == -INFINITY ? 0.f : exp2_fast(mw - M);
-            float ow = 0.f;
+            mw[w] = m_lds[w][h];
+            lw[w] = l_lds[w][h];
+            ow[w] = 0.f;
 #pragma unroll
-            for (int r = 0; r < ROWS; ++r) ow += o_lds[w][h][r][c];
-            O = fmaf(e, ow, O);
-            Lsum = fmaf(e, l_lds[w][h], Lsum);
-            bad |= __builtin_isnan(l_lds[w][h]);
+            for (int r = 0; r < ROWS; ++r) ow[w] += o_lds[w][h][r][c];
+            M[u] = fmaxf(M[u], mw[w]);
         }
-        if (p.n_split == 1) {
-            const float out = bad ? NAN : (M == -INFINITY ? 0.f : O / Lsum);
-            p.o[((size_t)b * p.Hq + h0 + h) * DV + c] = (uint16_t)(pack_bf16(out, 0.f) & 0xffffu);
-        } else {
-            // this split's partial; written and read with agent-scope atomic
-            // accesses (coherent across the XCDs' separate L2 caches without an
-            // L2 write-back)
-            float* dst = p.ws + (((size_t)b * p.Hq + h0 + h) * p.n_split + split) * ws_row;
-            store_coherent(dst + c, O);
-            if (c == 0) {
-                store_coherent(dst + DV, M);
-                store_coherent(dst + DV + 1, bad ? NAN : Lsum);
-            }
+#pragma unroll
+        for (int w = 0; w < kDecodeWaves; ++w) {
+            const float e = mw[w] == -INFINITY ? 0.f : exp2_fast(mw[w] - M[u]);
+            O[u] = fmaf(e, ow[w], O[u]);
+            Lsum[u] = fmaf(e, lw[w], Lsum[u]);
+            bad[u] |= __builtin_isnan(lw[w]);
         }
     }
-    if (p.n_split == 1) return;
+    if (p.n_split == 1) {
+#pragma unroll
+        for (int u = 0; u < kOut; ++u) {
+            const int idx = threadIdx.x + u * kDecodeThreads;
+            if (idx >= HG * DV) continue;
+            const int h = idx / DV, c = idx % DV;
+            const float out = bad[u] ? NAN : (M[u] == -INFINITY ? 0.f : O[u] / Lsum[u]);
+            p.o[((size_t)b * p.Hq + h0 + h) * DV + c] = (uint16_t)(pack_bf16(out, 0.f) & 0xffffu);
+        }
+        return;
+    }
+    // Otherwise write this split's partial. Partials are written and read with
+    // agent-scope atomic accesses (coherent across the XCDs' separate L2
+    // caches without an L2 write-back).
+#pragma unroll
+    for (int u = 0; u < kOut; ++u) {
+        const int idx = threadIdx.x + u * kDecodeThreads;
+        if (idx >= HG * DV) continue;
+        const int h = idx / DV, c = idx % DV;
+        float* dst = p.ws + (((size_t)b * p.Hq + h0 + h) * p.n_split + split) * ws_row;
+        store_coherent(dst + c, O[u]);
+        if (c == 0) {
+            store_coherent(dst + DV, M[u]);
+            store_coherent(dst + DV + 1, bad[u] ? NAN : Lsum[u]);
+        }
+    }
 
     // ---- the last workgroup of this (sequence, head group) to finish merges the
     // splits with the log-sum-exp rule and writes the bf16 output rows
@@ -543,43 +568,61 @@ __global__ __launch_bounds__(kDecodeThreads, (decode_min_blocks<HG, KF>())) void
                   (unsigned)(p.n_split - 1);
     __syncthreads();
     if (!is_last) return;
-    // one pass over the splits, up to 8 at a time (their loads in flight
-    // together), with the running-maximum rule of the online softmax
-    for (int idx = threadIdx.x; idx < HG * DV; idx += kDecodeThreads) {
-        const int h = idx / DV, c = idx % DV;
-        const float* base = p.ws + ((size_t)b * p.Hq + h0 + h) * p.n_split * ws_row;
-        float M = -INFINITY, O = 0.f, Lsum = 0.f;
-        bool bad = false;
-        for (int s0 = 0; s0 < p.n_split; s0 += 8) {
-            const int cnt = p.n_split - s0 < 8 ? p.n_split - s0 : 8;
-            float ms[8], ls[8], os[8];
+    // one pass over the splits, up to 8 at a time; all loads of a group, for
+    // every column this thread owns, are in flight together; the running-maximum
+    // rule of the online softmax combines them
+#pragma unroll
+    for (int u = 0; u < kOut; ++u) {
+        M[u] = -INFINITY;
+        O[u] = 0.f;
+        Lsum[u] = 0.f;
+        bad[u] = false;
+    }
+    for (int s0 = 0; s0 < p.n_split; s0 += 8) {
+        const int cnt = p.n_split - s0 < 8 ? p.n_split - s0 : 8;
+        float ms[kOut][8], ls[kOut][8], os[kOut][8];
+#pragma unroll
+        for (int u = 0; u < kOut; ++u) {
+            const int idx = threadIdx.x + u * kDecodeThreads;
+            if (idx >= HG * DV) continue;
+            const int h = idx / DV, c = idx % DV;
+            const float* base = p.ws + ((size_t)b * p.Hq + h0 + h) * p.n_split * ws_row;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 if (i < cnt) {
                     const float* part = base + (size_t)(s0 + i) * ws_row;
-                    ms[i] = load_coherent(part + DV);
-                    ls[i] = load_coherent(part + DV + 1);
-                    os[i] = load_coherent(part + c);
+                    ms[u][i] = load_coherent(part + DV);
+                    ls[u][i] = load_coherent(part + DV + 1);
+                    os[u][i] = load_coherent(part + c);
                 }
-            }
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                if (i >= cnt) break;
-                bad |= __builtin_isnan(ls[i]);
-                if (ms[i] == -INFINITY) continue;
-                if (ms[i] > M) {
-                    const float alpha = exp2_fast(M - ms[i]);
-                    O *= alpha;
-                    Lsum *= alpha;
-                    M = ms[i];
-                }
-                const float e = exp2_fast(ms[i] - M);
-                O = fmaf(e, os[i], O);
-                Lsum = fmaf(e, ls[i], Lsum);
             }
         }
+#pragma unroll
+        for (int u = 0; u < kOut; ++u) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                if (i >= cnt || threadIdx.x + u * kDecodeThreads >= HG * DV) break;
+                bad[u] |= __builtin_isnan(ls[u][i]);
+                if (ms[u][i] == -INFINITY) continue;
+                if (ms[u][i] > M[u]) {
+                    const float alpha = exp2_fast(M[u] - ms[u][i]);
+                    O[u] *= alpha;
+                    Lsum[u] *= alpha;
+                    M[u] = ms[u][i];
+                }
+                const float e = exp2_fast(ms[u][i] - M[u]);
+                O[u] = fmaf(e, os[u][i], O[u]);
+                Lsum[u] = fmaf(e, ls[u][i], Lsum[u]);
+            }
+        }
+    }
+#pragma unroll
+    for (int u = 0; u < kOut; ++u) {
+        const int idx = threadIdx.x + u * kDecodeThreads;
+        if (idx >= HG * DV) continue;
+        const int h = idx / DV, c = idx % DV;
         // no visible token -> zeros; a flagged bad block-table entry -> NaN
-        const float out = bad ? NAN : (M == -INFINITY ? 0.f : O / Lsum);
+        const float out = bad[u] ? NAN : (M[u] == -INFINITY ? 0.f : O[u] / Lsum[u]);
         p.o[((size_t)b * p.Hq + h0 + h) * DV + c] = (uint16_t)(pack_bf16(out, 0.f) & 0xffffu);
     }
     if (threadIdx.x == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -603,8 +646,12 @@ DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV) {
     long split_quanta = quanta > 0 ? (quanta + n_split - 1) / n_split : 1;
     pl.split_len = (int)(split_quanta * 256);
     pl.n_split = max_ctx > 0 ? (int)((max_ctx + pl.split_len - 1) / pl.split_len) : 1;
-    // one counter per (sequence, query head) covers any head grouping chosen at launch
-    pl.counter_bytes = ((size_t)B * Hq * sizeof(unsigned) + 255) / 256 * 256;
+    // One arrival counter per (sequence, head group). They are used only when
+    // the context is split, which needs fewer than TARGET_GROUPS pairs (fewer
+    // than twice that after a launch halves the head group), so one fixed
+    // leading region serves every shape: counters never land where another
+    // shape's call kept its partials, and a workspace can move between shapes.
+    pl.counter_bytes = kCounterRegionBytes;
     pl.ws_bytes = pl.counter_bytes + (size_t)B * Hq * pl.n_split * (DV + 2) * sizeof(float);
     return pl;
 }

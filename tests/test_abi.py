@@ -99,11 +99,14 @@ def test_workspace_query_is_pure_and_sized():
     ws = tb.tk_attn_decode_workspace_bytes
     a = ws(16, 32, 8, 4096, 128)
     assert a == ws(16, 32, 8, 4096, 128) > 0
-    counters = 2048                                           # 16 x 32 arrival counters (4 B), padded to 256
-    assert (a - counters) % (16 * 32 * 130 * 4) == 0          # + [B, Hq, n_split, d_v + 2] fp32
+    # a fixed leading region of 512 arrival counters (4 B) for every shape, then
+    # [B, Hq, n_split, d_v + 2] fp32 partials
+    counters = 2048
+    assert (a - counters) % (16 * 32 * 130 * 4) == 0
     assert ws(16, 30, 8, 4096, 128) == 0 and ws(0, 32, 8, 4096, 128) == 0
     assert ws(8, 32, 8, 131072, 128) >= 8 * 32 * 130 * 4
-    assert ws(1, 32, 8, 0, 128) == 256 + 32 * 130 * 4         # empty caches: one split, 32 counters
+    assert ws(1, 32, 8, 0, 128) == counters + 32 * 130 * 4      # empty caches: one split
+    assert ws(200, 64, 8, 64, 64) == counters + 200 * 64 * 66 * 4  # many pairs: one split
 
 
 def append(**kw):
