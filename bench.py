@@ -51,7 +51,9 @@ def parse():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200, help="timed steps")
-    ap.add_argument("--warmup", type=int, default=10, help="untimed warm-up steps")
+    ap.add_argument("--warmup", type=int, default=500,
+                    help="untimed warm-up steps (enough for the GPU to reach its steady clocks; the "
+                         "secondary workloads take a tenth of it, prefill at most 3)")
     ap.add_argument("--rotate", type=int, default=8, help="cache copies cycled through in the timed loop")
     ap.add_argument("--only", default=None, help="time just this workload (e.g. for profiling)")
     ap.add_argument("--no-secondary", action="store_true")
@@ -278,7 +280,7 @@ def main():
             big = spec.batch * spec.h_kv * spec.ctx * (spec.r + spec.d_v) * 2 > (1 << 30)
             calls = decode_setup(spec, dev, 1 if big else args.rotate)
             steps = args.steps if main else max(10, args.steps // 10)
-            res = decode_result(name, spec, calls, steps, args.warmup)
+            res = decode_result(name, spec, calls, steps, args.warmup if main else max(10, args.warmup // 10))
             res["rotate"] = len(calls)
             del calls
             torch.cuda.empty_cache()
