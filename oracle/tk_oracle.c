@@ -225,3 +225,114 @@ int tko_decode(const void* Q, int q_dt, const void* K, int k_dt, const float* k_
     }
     return 0;
 }
+
+/*
+ * Gradients of the causal (or full) prefill attention with respect to Q, K and
+ * V, for the thin-key training path (the paper trains thin-key models from
+ * scratch, Sec. 3). Written from the chain rule through the definition above,
+ * with the GQA grouping g = h / (H_q / H_kv):
+ *
+ *     P[h,i,j]  = exp(s[h,i,j] - lse[h,i]),  lse[h,i] = log sum_j exp(s[h,i,j])
+ *     dP[h,i,j] = sum_c dO[h,i,c] * V[g,j,c]
+ *     D[h,i]    = sum_j P[h,i,j] * dP[h,i,j]
+ *     dS[h,i,j] = P[h,i,j] * (dP[h,i,j] - D[h,i])
+ *     dQ[h,i,:] = scale * sum_j dS[h,i,j] * K[g,j,:]
+ *     dK[g,j,:] = scale * sum_{h in g} sum_i dS[h,i,j] * Q[h,i,:]
+ *     dV[g,j,:] = sum_{h in g} sum_i P[h,i,j] * dO[h,i,:]
+ *
+ * (D is the sum of P * dP over the row; it equals the sum of dO * O, which a
+ * GPU computes from the forward output.) Phase 1 goes row by row (lse, D, dQ),
+ * phase 2 key row by key row (dK, dV), recomputing scores as needed, all in
+ * fp64 from the exact widening of the inputs.
+ *
+ * Only query rows i >= row_lo are processed: dQ and lse of those rows are
+ * exact, and dK, dV hold the contributions of those rows only, which for a
+ * causal mask is the whole gradient of keys j >= row_lo + (Sk - Sq). row_lo = 0
+ * gives the full gradients. dQ [B,Hq,Sq,r], dK [B,Hkv,Sk,r], dV [B,Hkv,Sk,dv],
+ * lse [B,Hq,Sq] (natural logarithm) are fp64 and written (rows below row_lo of
+ * dQ and lse are left untouched). Returns 0, or -1 on bad shapes.
+ */
+int tko_prefill_backward(const void* Q, int q_dt, const void* K, int k_dt, const void* V, int v_dt,
+                         const void* dO, int do_dt, double* dQ, double* dK, double* dV, double* lse,
+                         long B, long Hq, long Hkv, long Sq, long Sk, long r, long dv,
+                         int causal, double scale, long row_lo, int threads) {
+    if (B < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv || Sq < 0 || Sk <= 0 || r <= 0 || dv <= 0) return -1;
+    if ((causal && Sq > Sk) || row_lo < 0) return -1;
+    const long G = Hq / Hkv, off = Sk - Sq;
+    set_threads(threads);
+    double* Dr = (double*)malloc(sizeof(double) * (size_t)(B * Hq * (Sq > 0 ? Sq : 1)));
+    if (!Dr) return -1;
+
+    /* phase 1: per query row, the log-sum-exp, D and dQ */
+    const long n_rows = B * Hq * Sq;
+#pragma omp parallel
+    {
+        double* s = (double*)malloc(sizeof(double) * (size_t)Sk);
+        double* dp = (double*)malloc(sizeof(double) * (size_t)Sk);
+#pragma omp for schedule(dynamic, 8)
+        for (long idx = 0; idx < n_rows; idx++) {
+            const long i = idx % Sq, h = (idx / Sq) % Hq, b = idx / (Sq * Hq), g = h / G;
+            if (i < row_lo) continue;
+            const long n = causal ? i + off + 1 : Sk;
+            const size_t kv0 = (size_t)(b * Hkv + g) * Sk;
+            double m = -INFINITY;
+            for (long j = 0; j < n; j++) {
+                double acc = 0.0;
+                for (long c = 0; c < r; c++)
+                    acc += ld(Q, q_dt, (size_t)idx * r + c) * ld(K, k_dt, (kv0 + j) * r + c);
+                s[j] = acc * scale;
+                if (s[j] > m) m = s[j];
+            }
+            double l = 0.0;
+            for (long j = 0; j < n; j++) l += exp(s[j] - m);
+            const double ls = m + log(l);
+            lse[idx] = ls;
+            double D = 0.0;
+            for (long j = 0; j < n; j++) {
+                double acc = 0.0;
+                for (long c = 0; c < dv; c++)
+                    acc += ld(dO, do_dt, (size_t)idx * dv + c) * ld(V, v_dt, (kv0 + j) * dv + c);
+                dp[j] = acc;
+                s[j] = exp(s[j] - ls); /* now P */
+                D += s[j] * dp[j];
+            }
+            Dr[idx] = D;
+            for (long c = 0; c < r; c++) dQ[(size_t)idx * r + c] = 0.0;
+            for (long j = 0; j < n; j++) {
+                const double ds = s[j] * (dp[j] - D);
+                for (long c = 0; c < r; c++) dQ[(size_t)idx * r + c] += scale * ds * ld(K, k_dt, (kv0 + j) * r + c);
+            }
+        }
+        free(s);
+        free(dp);
+    }
+
+    /* phase 2: per key row, dK and dV summed over the group's heads and rows */
+    const long n_keys = B * Hkv * Sk;
+#pragma omp parallel for schedule(dynamic, 8)
+    for (long kidx = 0; kidx < n_keys; kidx++) {
+        const long j = kidx % Sk, g = (kidx / Sk) % Hkv, b = kidx / (Sk * Hkv);
+        double* dk = dK + (size_t)kidx * r;
+        double* dvv = dV + (size_t)kidx * dv;
+        for (long c = 0; c < r; c++) dk[c] = 0.0;
+        for (long c = 0; c < dv; c++) dvv[c] = 0.0;
+        long i0 = causal ? j - off : 0;
+        if (i0 < row_lo) i0 = row_lo;
+        if (i0 < 0) i0 = 0;
+        for (long h = g * G; h < (g + 1) * G; h++) {
+            for (long i = i0; i < Sq; i++) {
+                const size_t idx = (size_t)((b * Hq + h) * Sq + i);
+                double acc = 0.0;
+                for (long c = 0; c < r; c++) acc += ld(Q, q_dt, idx * r + c) * ld(K, k_dt, (size_t)kidx * r + c);
+                const double p = exp(scale * acc - lse[idx]);
+                double dpv = 0.0;
+                for (long c = 0; c < dv; c++) dpv += ld(dO, do_dt, idx * dv + c) * ld(V, v_dt, (size_t)kidx * dv + c);
+                const double ds = p * (dpv - Dr[idx]);
+                for (long c = 0; c < r; c++) dk[c] += scale * ds * ld(Q, q_dt, idx * r + c);
+                for (long c = 0; c < dv; c++) dvv[c] += p * ld(dO, do_dt, idx * dv + c);
+            }
+        }
+    }
+    free(Dr);
+    return 0;
+}

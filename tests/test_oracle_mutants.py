@@ -40,9 +40,28 @@ MUTANTS = {
     "bf16_widening": ("uint32_t w = (uint32_t)bits << 16;", "uint32_t w = ((uint32_t)bits << 16) | 0x8000u;"),
 }
 
+# slips in the backward, each caught by tests/test_oracle_backward.py
+BACKWARD_MUTANTS = {
+    "bwd_dq_D_dropped": ("const double ds = s[j] * (dp[j] - D);", "const double ds = s[j] * dp[j];"),
+    "bwd_dk_D_dropped": ("const double ds = p * (dpv - Dr[idx]);", "const double ds = p * dpv;"),
+    "bwd_dq_scale_dropped": ("dQ[(size_t)idx * r + c] += scale * ds *", "dQ[(size_t)idx * r + c] += ds *"),
+    "bwd_dk_uses_key": ("dk[c] += scale * ds * ld(Q, q_dt, idx * r + c);",
+                        "dk[c] += scale * ds * ld(K, k_dt, (size_t)kidx * r + c);"),
+    "bwd_dv_unnormalised": ("const double p = exp(scale * acc - lse[idx]);", "const double p = exp(scale * acc);"),
+    "bwd_causal_rows": ("long i0 = causal ? j - off : 0;", "long i0 = causal ? j - off + 1 : 0;"),
+    "bwd_gqa_one_head": ("for (long h = g * G; h < (g + 1) * G; h++) {",
+                         "for (long h = g * G; h < g * G + 1; h++) {"),
+    "bwd_lse_max_only": ("const double ls = m + log(l);", "const double ls = m;"),
+    "bwd_score_scale_dropped": ("s[j] = acc * scale;", "s[j] = acc;"),
+    "bwd_dv_value_row": ("dvv[c] += p * ld(dO, do_dt, idx * dv + c);",
+                         "dvv[c] += p * ld(V, v_dt, (size_t)kidx * dv + c);"),
+}
+PIN_FILES = {**{n: "test_oracle_pins.py" for n in MUTANTS}, **{n: "test_oracle_backward.py" for n in BACKWARD_MUTANTS}}
+ALL_MUTANTS = {**MUTANTS, **BACKWARD_MUTANTS}
+
 
 def run_mutant(name, tmp):
-    old, new = MUTANTS[name]
+    old, new = ALL_MUTANTS[name]
     src = open(SRC).read()
     assert src.count(old) == 1, name
     path = os.path.join(tmp, f"{name}.c")
@@ -52,7 +71,7 @@ def run_mutant(name, tmp):
     subprocess.check_call(["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-o", lib, path, "-lm"])
     env = dict(os.environ, TKO_ORACLE_LIB=lib, OMP_NUM_THREADS="1")
     p = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                        os.path.join(ROOT, "tests", PIN_FILES[name])],
                        env=env, cwd=ROOT, capture_output=True, text=True, timeout=600)
     return name, p.returncode
 
@@ -60,7 +79,7 @@ def run_mutant(name, tmp):
 def test_every_mutant_is_caught():
     with tempfile.TemporaryDirectory() as tmp:
         with cf.ThreadPoolExecutor(max_workers=6) as ex:
-            results = list(ex.map(lambda n: run_mutant(n, tmp), MUTANTS))
+            results = list(ex.map(lambda n: run_mutant(n, tmp), ALL_MUTANTS))
     survivors = [n for n, rc in results if rc == 0]
     errors = [(n, rc) for n, rc in results if rc not in (0, 1)]
     assert not errors, errors
