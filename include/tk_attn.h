@@ -73,6 +73,61 @@ tk_status tk_attn_prefill(const void* Q, const void* K, const void* V, void* O,
                           int causal, float scale, tk_dtype dtype, hipStream_t stream);
 
 /*
+ * Training forward: tk_attn_prefill for bf16 that also writes each query row's
+ * log-sum-exp, the statistic the backward pass recomputes the attention weights
+ * from (the weights of Eq. 4 are exp(scale q.k - lse)).
+ *
+ *   Q, K, V, O, shapes, causal, scale: as tk_attn_prefill, bf16 only.
+ *   lse [batch, H_q, seq_q] fp32 (written): natural log of the sum over the
+ *       row's visible keys of exp(scale * q.k), with the attention weights rounded
+ *       to bf16 as the kernel forms them (so it matches the normalisation of O).
+ * O is bitwise the output of tk_attn_prefill for the same arguments.
+ * Errors as tk_attn_prefill; lse == NULL is invalid; TK_F32 is unsupported.
+ */
+tk_status tk_attn_prefill_lse(const void* Q, const void* K, const void* V, void* O, float* lse,
+                              int batch, int H_q, int H_kv, int seq_q, int seq_k, int r, int d_v,
+                              int causal, float scale, hipStream_t stream);
+
+/*
+ * Bytes of device workspace tk_attn_prefill_backward needs: one fp32 per query
+ * row (D = rowsum(dO * O)), rounded up to 256. Returns 0 for invalid shapes.
+ */
+size_t tk_attn_prefill_backward_workspace_bytes(int batch, int H_q, int seq_q);
+
+/*
+ * Backward pass of the thin-key prefill: the gradients of the attention core of
+ * Eq. 4 with respect to the r-wide Q and K and the d_v-wide V, needed to train
+ * thin-key models from scratch (Sec. 3, Exp. 7 and 7b, whose shorter wall-clock
+ * comes from the smaller Q K^T work in both passes). With P the attention
+ * weights and D = rowsum(dO * O):
+ *     dV = P^T dO,   dS = P * (dO V^T - D),   dQ = scale dS K,   dK = scale dS^T Q
+ * where dK and dV sum over the H_q / H_kv query heads of each KV head.
+ *
+ *   Q [batch, H_q, seq_q, r]   K [batch, H_kv, seq_k, r]   V [batch, H_kv, seq_k, d_v]
+ *   O, dO [batch, H_q, seq_q, d_v]: the forward output and the loss gradient
+ *   lse [batch, H_q, seq_q] fp32: from tk_attn_prefill_lse with the same arguments
+ *   dQ [batch, H_q, seq_q, r], dK [batch, H_kv, seq_k, r],
+ *   dV [batch, H_kv, seq_k, d_v]: written (overwritten, not accumulated)
+ *   all tensors bf16 except lse; accumulation in fp32, one rounding per output.
+ *   workspace: device memory of at least
+ *       tk_attn_prefill_backward_workspace_bytes(batch, H_q, seq_q) bytes,
+ *       4-byte aligned, no initial contents required; calls sharing it must
+ *       not run concurrently.
+ * causal and scale as tk_attn_prefill. No atomics: results are bitwise
+ * reproducible. Keys that no row sees get zero gradients; seq_q == 0 with
+ * seq_k > 0 writes zero dK and dV; batch == 0 is a no-op.
+ * Supported: r in {32, 64, 128}; d_v in {64, 128}; H_q % H_kv == 0.
+ * Errors: TK_ERR_INVALID_ARG for null or misaligned (16 bytes) tensors or
+ * inconsistent shapes, TK_ERR_WORKSPACE for a missing or small workspace,
+ * TK_ERR_UNSUPPORTED for other r or d_v.
+ */
+tk_status tk_attn_prefill_backward(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                                   const float* lse, void* dQ, void* dK, void* dV,
+                                   int batch, int H_q, int H_kv, int seq_q, int seq_k, int r, int d_v,
+                                   int causal, float scale, void* workspace, size_t workspace_bytes,
+                                   hipStream_t stream);
+
+/*
  * Bytes of device workspace tk_attn_decode needs for these shapes (split-K
  * partial results). A pure function of its arguments: no device query.
  * Returns 0 for invalid shapes.

@@ -66,7 +66,7 @@ def lib():
         L.tko_int4_value.argtypes = [vp, ctypes.c_size_t]
         L.tko_int4_value.restype = d
         L.tko_max_threads.restype = i
-        L.tko_prefill_backward.argtypes = [vp, i, vp, i, vp, i, vp, i, vp, vp, vp, vp,
+        L.tko_prefill_backward.argtypes = [vp, i, vp, i, vp, i, vp, i, vp, i, vp, vp, vp, vp,
                                            l, l, l, l, l, l, l, i, d, l, i]
         L.tko_prefill_backward.restype = i
         _lib = L
@@ -158,10 +158,12 @@ def decode(q, k, v, ctx_lens, scale=None, k_scale=None, block_table=None, block_
     return o
 
 
-def prefill_backward(q, k, v, do, causal=True, scale=None, row_lo=0, threads=0):
+def prefill_backward(q, k, v, do, causal=True, scale=None, row_lo=0, threads=0, o=None):
     """Gradients (dQ [B,Hq,Sq,r], dK [B,Hkv,Sk,r], dV [B,Hkv,Sk,dv]) of the prefill
     attention for the output gradient dO [B,Hq,Sq,dv], and the forward's
     log-sum-exp [B,Hq,Sq] (natural log), all fp64; see ``tko_prefill_backward``.
+    ``o`` (optional, [B,Hq,Sq,dv]): a stored forward output whose rowsum(dO * O)
+    is used as D (by default D is the exact sum of P * dP).
     Only query rows >= row_lo are processed (dQ and lse of lower rows are NaN, and
     dK, dV hold those rows' contributions: for a causal mask the full gradient of
     keys >= row_lo + Sk - Sq)."""
@@ -174,12 +176,13 @@ def prefill_backward(q, k, v, do, causal=True, scale=None, row_lo=0, threads=0):
     pk, ck, k_ = _typed(k)
     pv, cv, v_ = _typed(v)
     pd, cd, d_ = _typed(do)
+    po, co, o_ = (None, 0, None) if o is None else _typed(o)
     dq = torch.full((B, Hq, Sq, r), float("nan"), dtype=torch.float64)
     dk = torch.empty(B, Hkv, Sk, r, dtype=torch.float64)
     dvv = torch.empty(B, Hkv, Sk, dv, dtype=torch.float64)
     lse = torch.full((B, Hq, Sq), float("nan"), dtype=torch.float64)
     ptr = lambda t: ctypes.c_void_p(t.data_ptr())
-    rc = lib().tko_prefill_backward(pq, cq, pk, ck, pv, cv, pd, cd, ptr(dq), ptr(dk), ptr(dvv), ptr(lse),
+    rc = lib().tko_prefill_backward(pq, cq, pk, ck, pv, cv, pd, cd, po, co, ptr(dq), ptr(dk), ptr(dvv), ptr(lse),
                                     B, Hq, Hkv, Sq, Sk, r, dv, int(bool(causal)), float(scale), int(row_lo),
                                     int(threads))
     if rc != 0:

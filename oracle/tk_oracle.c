@@ -240,8 +240,11 @@ int tko_decode(const void* Q, int q_dt, const void* K, int k_dt, const float* k_
  *     dK[g,j,:] = scale * sum_{h in g} sum_i dS[h,i,j] * Q[h,i,:]
  *     dV[g,j,:] = sum_{h in g} sum_i P[h,i,j] * dO[h,i,:]
  *
- * (D is the sum of P * dP over the row; it equals the sum of dO * O, which a
- * GPU computes from the forward output.) Phase 1 goes row by row (lse, D, dQ),
+ * D is the sum of P * dP over the row, which equals the sum of dO * O for the
+ * exact forward output O. When O is given (not NULL), D is instead taken as
+ * sum_c dO[h,i,c] * O[h,i,c] of that O: the form of the backward pass that is
+ * handed the forward output as stored (rounded), which then enters D, and
+ * through D the query and key gradients. Phase 1 goes row by row (lse, D, dQ),
  * phase 2 key row by key row (dK, dV), recomputing scores as needed, all in
  * fp64 from the exact widening of the inputs.
  *
@@ -253,7 +256,8 @@ int tko_decode(const void* Q, int q_dt, const void* K, int k_dt, const float* k_
  * dQ and lse are left untouched). Returns 0, or -1 on bad shapes.
  */
 int tko_prefill_backward(const void* Q, int q_dt, const void* K, int k_dt, const void* V, int v_dt,
-                         const void* dO, int do_dt, double* dQ, double* dK, double* dV, double* lse,
+                         const void* dO, int do_dt, const void* O, int o_dt, double* dQ, double* dK, double* dV,
+                         double* lse,
                          long B, long Hq, long Hkv, long Sq, long Sk, long r, long dv,
                          int causal, double scale, long row_lo, int threads) {
     if (B < 0 || Hq <= 0 || Hkv <= 0 || Hq % Hkv || Sq < 0 || Sk <= 0 || r <= 0 || dv <= 0) return -1;
@@ -295,6 +299,11 @@ int tko_prefill_backward(const void* Q, int q_dt, const void* K, int k_dt, const
                 dp[j] = acc;
                 s[j] = exp(s[j] - ls); /* now P */
                 D += s[j] * dp[j];
+            }
+            if (O) {
+                D = 0.0;
+                for (long c = 0; c < dv; c++)
+                    D += ld(dO, do_dt, (size_t)idx * dv + c) * ld(O, o_dt, (size_t)idx * dv + c);
             }
             Dr[idx] = D;
             for (long c = 0; c < r; c++) dQ[(size_t)idx * r + c] = 0.0;

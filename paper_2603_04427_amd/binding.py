@@ -23,6 +23,10 @@ TK_F32, TK_BF16, TK_FP8_E4M3, TK_INT4 = 0, 1, 2, 3
 _vp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
 SIGNATURES = {
     "tk_attn_prefill": ([_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _f, _i, _vp], _i),
+    "tk_attn_prefill_lse": ([_vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _f, _vp], _i),
+    "tk_attn_prefill_backward_workspace_bytes": ([_i, _i, _i], _sz),
+    "tk_attn_prefill_backward": ([_vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _i, _i, _f,
+                                  _vp, _sz, _vp], _i),
     "tk_attn_decode_workspace_bytes": ([_i, _i, _i, _i, _i], _sz),
     "tk_attn_decode": ([_vp, _vp, _vp, _vp, _i, _i, _i, _vp, _i, _i, _i, _f, _i, _vp, _vp, _i, _i, _i,
                         _vp, _sz, _vp], _i),
@@ -91,17 +95,18 @@ class PreparedCall:
     """A C entry point with its arguments marshalled once; calling it launches again
     with the same tensors (for timing loops and graph-free replay)."""
 
-    def __init__(self, name: str, args, keep):
+    def __init__(self, name: str, args, keep, result=None):
         self.name = name
         self.fn = getattr(lib(), name)
         self.args = args
         self.keep = keep  # tensors whose memory the pointers refer to
+        self.result = keep[-1] if result is None else result
 
     def __call__(self):
         st = self.fn(*self.args)
         if st != TK_OK:
             raise TkError(st, self.name)
-        return self.keep[-1]
+        return self.result
 
 
 def prepare_prefill(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, O: Optional[torch.Tensor] = None,
@@ -128,6 +133,83 @@ def tk_attn_prefill(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, O: Option
                     causal: bool = True, scale: float = 0.0, stream=None) -> torch.Tensor:
     """O = softmax(scale Q K^T [causal]) V for Q [B,Hq,Sq,r], K [B,Hkv,Sk,r], V [B,Hkv,Sk,dv]."""
     return prepare_prefill(Q, K, V, O, causal, scale, stream)()
+
+
+def _prefill_shapes(Q, K, V):
+    B, Hq, Sq, r = Q.shape
+    _, Hkv, Sk, dv = V.shape
+    if K.shape != (B, Hkv, Sk, r) or V.shape[0] != B:
+        raise ValueError(f"shape mismatch Q{tuple(Q.shape)} K{tuple(K.shape)} V{tuple(V.shape)}")
+    return B, Hq, Hkv, Sq, Sk, r, dv
+
+
+def prepare_prefill_lse(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, O: Optional[torch.Tensor] = None,
+                        lse: Optional[torch.Tensor] = None, causal: bool = True, scale: float = 0.0,
+                        stream=None) -> PreparedCall:
+    bf = (torch.bfloat16,)
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V")):
+        _check(t, n, bf, 4)
+    B, Hq, Hkv, Sq, Sk, r, dv = _prefill_shapes(Q, K, V)
+    if O is None:
+        O = torch.empty(B, Hq, Sq, dv, dtype=torch.bfloat16, device=Q.device)
+    if lse is None:
+        lse = torch.empty(B, Hq, Sq, dtype=torch.float32, device=Q.device)
+    _check(O, "O", bf, 4)
+    _check(lse, "lse", (torch.float32,), 3)
+    if O.shape != (B, Hq, Sq, dv) or lse.shape != (B, Hq, Sq):
+        raise ValueError("O or lse has the wrong shape")
+    args = (_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(lse), B, Hq, Hkv, Sq, Sk, r, dv, int(bool(causal)),
+            float(scale), _stream(stream))
+    return PreparedCall("tk_attn_prefill_lse", args, (Q, K, V, O, lse), result=(O, lse))
+
+
+def tk_attn_prefill_lse(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, O: Optional[torch.Tensor] = None,
+                        lse: Optional[torch.Tensor] = None, causal: bool = True, scale: float = 0.0,
+                        stream=None):
+    """bf16 prefill that also returns each row's log-sum-exp (fp32 [B, Hq, Sq]): (O, lse)."""
+    return prepare_prefill_lse(Q, K, V, O, lse, causal, scale, stream)()
+
+
+def tk_attn_prefill_backward_workspace_bytes(batch: int, H_q: int, seq_q: int) -> int:
+    return int(lib().tk_attn_prefill_backward_workspace_bytes(batch, H_q, seq_q))
+
+
+def prepare_prefill_backward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, O: torch.Tensor,
+                             dO: torch.Tensor, lse: torch.Tensor, causal: bool = True, scale: float = 0.0,
+                             dQ: Optional[torch.Tensor] = None, dK: Optional[torch.Tensor] = None,
+                             dV: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                             stream=None) -> PreparedCall:
+    bf = (torch.bfloat16,)
+    for t, n in ((Q, "Q"), (K, "K"), (V, "V"), (O, "O"), (dO, "dO")):
+        _check(t, n, bf, 4)
+    _check(lse, "lse", (torch.float32,), 3)
+    B, Hq, Hkv, Sq, Sk, r, dv = _prefill_shapes(Q, K, V)
+    if O.shape != (B, Hq, Sq, dv) or dO.shape != O.shape or lse.shape != (B, Hq, Sq):
+        raise ValueError("O, dO or lse has the wrong shape")
+    dQ = torch.empty_like(Q) if dQ is None else dQ
+    dK = torch.empty_like(K) if dK is None else dK
+    dV = torch.empty_like(V) if dV is None else dV
+    for t, n, ref in ((dQ, "dQ", Q), (dK, "dK", K), (dV, "dV", V)):
+        _check(t, n, bf, 4)
+        if t.shape != ref.shape:
+            raise ValueError(f"{n} has the wrong shape")
+    if workspace is None:
+        workspace = torch.empty(tk_attn_prefill_backward_workspace_bytes(B, Hq, Sq), dtype=torch.uint8,
+                                device=Q.device)
+    args = (_ptr(Q), _ptr(K), _ptr(V), _ptr(O), _ptr(dO), _ptr(lse), _ptr(dQ), _ptr(dK), _ptr(dV),
+            B, Hq, Hkv, Sq, Sk, r, dv, int(bool(causal)), float(scale), _ptr(workspace),
+            workspace.numel() * workspace.element_size(), _stream(stream))
+    return PreparedCall("tk_attn_prefill_backward", args, (Q, K, V, O, dO, lse, dQ, dK, dV, workspace),
+                        result=(dQ, dK, dV))
+
+
+def tk_attn_prefill_backward(Q: torch.Tensor, K: torch.Tensor, V: torch.Tensor, O: torch.Tensor,
+                             dO: torch.Tensor, lse: torch.Tensor, causal: bool = True, scale: float = 0.0,
+                             dQ: Optional[torch.Tensor] = None, dK: Optional[torch.Tensor] = None,
+                             dV: Optional[torch.Tensor] = None, workspace: Optional[torch.Tensor] = None,
+                             stream=None):
+    """Gradients (dQ, dK, dV) of the bf16 prefill given O, dO and the forward's lse."""
+    return prepare_prefill_backward(Q, K, V, O, dO, lse, causal, scale, dQ, dK, dV, workspace, stream)()
 
 
 def tk_attn_decode_workspace_bytes(batch: int, H_q: int, H_kv: int, max_ctx: int, d_v: int) -> int:

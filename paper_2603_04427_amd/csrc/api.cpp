@@ -25,6 +25,43 @@ constexpr long kMaxGrid = 65535;
 
 int key_format(tk_dtype k) { return k == TK_FP8_E4M3 ? 1 : (k == TK_INT4 ? 2 : 0); }
 
+tk_status prefill_impl(const void* Q, const void* K, const void* V, void* O, float* lse, int batch, int H_q,
+                       int H_kv, int seq_q, int seq_k, int r, int d_v, int causal, float scale, tk_dtype dtype,
+                       hipStream_t stream) {
+    if (batch < 0 || H_q <= 0 || H_kv <= 0 || seq_q < 0 || seq_k < 0 || r <= 0 || d_v <= 0)
+        return TK_ERR_INVALID_ARG;
+    if (H_q % H_kv != 0) return TK_ERR_INVALID_ARG;
+    if (dtype != TK_F32 && dtype != TK_BF16) return dtype == TK_FP8_E4M3 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
+    if (causal && seq_q > seq_k) return TK_ERR_INVALID_ARG;
+    if (batch == 0 || seq_q == 0) return TK_OK;
+    if (seq_k == 0) return TK_ERR_INVALID_ARG;
+    if (!Q || !K || !V || !O) return TK_ERR_INVALID_ARG;
+    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return TK_ERR_INVALID_ARG;
+    if (lse && ((uintptr_t)lse & 3u) != 0) return TK_ERR_INVALID_ARG;
+    if (!supported_r(r) || !supported_dv(d_v)) return TK_ERR_UNSUPPORTED;
+    const int G = H_q / H_kv;
+    const int hpw = (G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1);
+    const long bm = 32L * (4 / hpw);
+    if ((seq_q + bm - 1) / bm > 0x7fffffffL || (long)H_kv * (G / hpw) > kMaxGrid || batch > kMaxGrid)
+        return TK_ERR_UNSUPPORTED;
+
+    tk::PrefillParams p{};
+    p.q = Q;
+    p.k = K;
+    p.v = V;
+    p.o = O;
+    p.lse = lse;
+    p.B = batch;
+    p.Hq = H_q;
+    p.Hkv = H_kv;
+    p.G = G;
+    p.Sq = seq_q;
+    p.Sk = seq_k;
+    p.causal = causal ? 1 : 0;
+    p.qscale = resolve_scale(scale, r) * tk::kLog2e;
+    return dtype == TK_BF16 ? tk::launch_prefill_bf16(p, r, d_v, stream) : tk::launch_prefill_f32(p, r, d_v, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -45,27 +82,57 @@ int tk_version(void) { return 100; }  // 0.1.0
 tk_status tk_attn_prefill(const void* Q, const void* K, const void* V, void* O, int batch, int H_q, int H_kv,
                           int seq_q, int seq_k, int r, int d_v, int causal, float scale, tk_dtype dtype,
                           hipStream_t stream) {
+    return prefill_impl(Q, K, V, O, nullptr, batch, H_q, H_kv, seq_q, seq_k, r, d_v, causal, scale, dtype, stream);
+}
+
+tk_status tk_attn_prefill_lse(const void* Q, const void* K, const void* V, void* O, float* lse, int batch, int H_q,
+                              int H_kv, int seq_q, int seq_k, int r, int d_v, int causal, float scale,
+                              hipStream_t stream) {
+    if (!lse && batch > 0 && seq_q > 0) return TK_ERR_INVALID_ARG;
+    return prefill_impl(Q, K, V, O, lse, batch, H_q, H_kv, seq_q, seq_k, r, d_v, causal, scale, TK_BF16, stream);
+}
+
+size_t tk_attn_prefill_backward_workspace_bytes(int batch, int H_q, int seq_q) {
+    if (batch < 0 || H_q <= 0 || seq_q < 0) return 0;
+    size_t rows = (size_t)batch * (size_t)H_q * (size_t)seq_q;
+    rows = rows > 0 ? rows : 1;
+    return (rows * sizeof(float) + 255) / 256 * 256;
+}
+
+tk_status tk_attn_prefill_backward(const void* Q, const void* K, const void* V, const void* O, const void* dO,
+                                   const float* lse, void* dQ, void* dK, void* dV, int batch, int H_q, int H_kv,
+                                   int seq_q, int seq_k, int r, int d_v, int causal, float scale, void* workspace,
+                                   size_t workspace_bytes, hipStream_t stream) {
     if (batch < 0 || H_q <= 0 || H_kv <= 0 || seq_q < 0 || seq_k < 0 || r <= 0 || d_v <= 0)
         return TK_ERR_INVALID_ARG;
     if (H_q % H_kv != 0) return TK_ERR_INVALID_ARG;
-    if (dtype != TK_F32 && dtype != TK_BF16) return dtype == TK_FP8_E4M3 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
     if (causal && seq_q > seq_k) return TK_ERR_INVALID_ARG;
-    if (batch == 0 || seq_q == 0) return TK_OK;
-    if (seq_k == 0) return TK_ERR_INVALID_ARG;
-    if (!Q || !K || !V || !O) return TK_ERR_INVALID_ARG;
-    if (!aligned16(Q) || !aligned16(K) || !aligned16(V) || !aligned16(O)) return TK_ERR_INVALID_ARG;
-    if (!supported_r(r) || !supported_dv(d_v)) return TK_ERR_UNSUPPORTED;
+    if (seq_k == 0 && seq_q > 0) return TK_ERR_INVALID_ARG;
+    if (batch == 0 || seq_k == 0) return TK_OK;
+    if (!K || !V || !dK || !dV) return TK_ERR_INVALID_ARG;
+    if (seq_q > 0 && (!Q || !O || !dO || !lse || !dQ)) return TK_ERR_INVALID_ARG;
+    if (!aligned16(K) || !aligned16(V) || !aligned16(dK) || !aligned16(dV)) return TK_ERR_INVALID_ARG;
+    if (seq_q > 0 && (!aligned16(Q) || !aligned16(O) || !aligned16(dO) || !aligned16(dQ) ||
+                      ((uintptr_t)lse & 3u) != 0))
+        return TK_ERR_INVALID_ARG;
+    if (!workspace || ((uintptr_t)workspace & 3u) != 0 ||
+        workspace_bytes < tk_attn_prefill_backward_workspace_bytes(batch, H_q, seq_q))
+        return TK_ERR_WORKSPACE;
+    if ((r != 32 && r != 64 && r != 128) || !supported_dv(d_v)) return TK_ERR_UNSUPPORTED;
     const int G = H_q / H_kv;
-    const int hpw = (G % 4 == 0) ? 4 : (G % 2 == 0 ? 2 : 1);
-    const long bm = 32L * (4 / hpw);
-    if ((seq_q + bm - 1) / bm > 0x7fffffffL || (long)H_kv * (G / hpw) > kMaxGrid || batch > kMaxGrid)
-        return TK_ERR_UNSUPPORTED;
+    if ((long)batch * H_q * (long)(seq_q > seq_k ? seq_q : seq_k) > 0x7fffffffL) return TK_ERR_UNSUPPORTED;
 
-    tk::PrefillParams p{};
+    tk::PrefillBwdParams p{};
     p.q = Q;
     p.k = K;
     p.v = V;
     p.o = O;
+    p.dout = dO;
+    p.lse = lse;
+    p.dq = dQ;
+    p.dk = dK;
+    p.dv = dV;
+    p.delta = (float*)workspace;
     p.B = batch;
     p.Hq = H_q;
     p.Hkv = H_kv;
@@ -73,8 +140,9 @@ tk_status tk_attn_prefill(const void* Q, const void* K, const void* V, void* O, 
     p.Sq = seq_q;
     p.Sk = seq_k;
     p.causal = causal ? 1 : 0;
-    p.qscale = resolve_scale(scale, r) * tk::kLog2e;
-    return dtype == TK_BF16 ? tk::launch_prefill_bf16(p, r, d_v, stream) : tk::launch_prefill_f32(p, r, d_v, stream);
+    p.scale = resolve_scale(scale, r);
+    p.qscale = p.scale * tk::kLog2e;
+    return tk::launch_prefill_backward(p, r, d_v, stream);
 }
 
 size_t tk_attn_decode_workspace_bytes(int batch, int H_q, int H_kv, int max_ctx, int d_v) {

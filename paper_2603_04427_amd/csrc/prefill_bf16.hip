@@ -417,12 +417,15 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_ke
         __syncthreads();
     }
 
-    // ---- epilogue: normalise and store bf16 rows
+    // ---- epilogue: normalise and store bf16 rows (and, when asked, the row's
+    // log-sum-exp: the reference maximum plus log2 of the sum, in natural log)
 #pragma unroll
     for (int qc = 0; qc < QC; ++qc) {
         const float ltot = xor32_sum(lsum[qc]);
         const float inv = 1.f / ltot;
         const int qrow = qw0 + 32 * qc + col;
+        if (p.lse != nullptr && half == 0 && qrow < p.Sq)
+            p.lse[((size_t)b * p.Hq + h) * p.Sq + qrow] = (m_ref[qc] + __builtin_amdgcn_logf(ltot)) * kLn2;
         if (qrow < p.Sq) {
             uint16_t* orow = og + (size_t)qrow * DV;
 #pragma unroll

@@ -10,6 +10,7 @@
 namespace tk {
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
 
 // Key formats of the cache: bf16 rows, OCP E4M3 codes, or 4-bit integer codes
 // (excess-8 nibbles, two per byte, low nibble first); the quantised formats
@@ -68,10 +69,31 @@ struct PrefillParams {
     const void* k;   // [B, Hkv, Sk, R]
     const void* v;   // [B, Hkv, Sk, DV]
     void* o;         // [B, Hq, Sq, DV]
+    float* lse;      // [B, Hq, Sq] natural-log log-sum-exp of the scaled scores, or null (bf16 only)
     int B, Hq, Hkv, G, Sq, Sk;
     int causal;
     float qscale;    // softmax scale * log2(e)
 };
+
+// Prefill backward (bf16): dQ with D = rowsum(dO * O), then dK and dV.
+struct PrefillBwdParams {
+    const void* q;      // [B, Hq, Sq, R]
+    const void* k;      // [B, Hkv, Sk, R]
+    const void* v;      // [B, Hkv, Sk, DV]
+    const void* o;      // [B, Hq, Sq, DV]   forward output
+    const void* dout;   // [B, Hq, Sq, DV]   gradient of the output
+    const float* lse;   // [B, Hq, Sq]       forward log-sum-exp (natural log)
+    void* dq;           // [B, Hq, Sq, R]
+    void* dk;           // [B, Hkv, Sk, R]
+    void* dv;           // [B, Hkv, Sk, DV]
+    float* delta;       // [B, Hq, Sq] workspace: D of each row
+    int B, Hq, Hkv, G, Sq, Sk;
+    int causal;
+    float scale;        // softmax scale
+    float qscale;       // scale * log2(e)
+};
+
+tk_status launch_prefill_backward(const PrefillBwdParams& p, int R, int DV, hipStream_t stream);
 
 tk_status launch_prefill_bf16(const PrefillParams& p, int R, int DV, hipStream_t stream);
 tk_status launch_prefill_f32(const PrefillParams& p, int R, int DV, hipStream_t stream);

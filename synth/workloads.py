@@ -29,7 +29,7 @@ from .gen import normal, permutation, stream_key, uniform_int
 E4M3_MAX = 448.0
 
 # tensor ids inside one workload's seed family
-T_Q, T_K, T_V, T_PERM, T_STRUCT = 0, 1, 2, 3, 4
+T_Q, T_K, T_V, T_PERM, T_STRUCT, T_DO = 0, 1, 2, 3, 4, 5
 
 
 @dataclass(frozen=True)
@@ -176,6 +176,13 @@ def make_prefill(spec: PrefillSpec, device="cpu", structured: bool = False):
         q[:, :, rows[ok]] = lam * kk[:, :, src[ok]]
         del kk, i0
     return {"q": q.to(dt), "k": k, "v": v.to(dt)}
+
+
+def make_prefill_grad(spec: PrefillSpec, device="cpu"):
+    """The loss gradient dO [B, Hq, Sq, dv] of a prefill workload for the backward
+    pass: i.i.d. N(0, 1) entries in the workload's dtype."""
+    dt = torch.float32 if spec.dtype == "f32" else torch.bfloat16
+    return _draw(spec.config_id, T_DO, (spec.batch, spec.h_q, spec.seq_q, spec.d_v), device).to(dt)
 
 
 def _to_pages(x: torch.Tensor, table: torch.Tensor, bs: int, n_blocks: int) -> torch.Tensor:

@@ -62,6 +62,59 @@ def test_prefill_validation(kw, status):
     assert prefill(**kw) == status
 
 
+def prefill_lse(**kw):
+    a = dict(Q=P, K=P, V=P, O=P, lse=P, batch=1, H_q=4, H_kv=2, seq_q=8, seq_k=8, r=32, d_v=128, causal=1,
+             scale=0.0, stream=None)
+    a.update(kw)
+    return tb.lib().tk_attn_prefill_lse(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(lse=None), tb.TK_ERR_INVALID_ARG),
+    (dict(lse=ctypes.c_void_p(0x10002)), tb.TK_ERR_INVALID_ARG),   # not 4-byte aligned
+    (dict(H_q=3), tb.TK_ERR_INVALID_ARG),
+    (dict(seq_q=9), tb.TK_ERR_INVALID_ARG),
+    (dict(r=24), tb.TK_ERR_UNSUPPORTED),
+    (dict(seq_q=0, lse=None), tb.TK_OK),
+])
+def test_prefill_lse_validation(kw, status):
+    assert prefill_lse(**kw) == status
+
+
+def backward(**kw):
+    a = dict(Q=P, K=P, V=P, O=P, dO=P, lse=P, dQ=P, dK=P, dV=P, batch=1, H_q=4, H_kv=2, seq_q=8, seq_k=8,
+             r=32, d_v=128, causal=1, scale=0.0, ws=P, ws_bytes=1 << 20, stream=None)
+    a.update(kw)
+    return tb.lib().tk_attn_prefill_backward(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H_q=3), tb.TK_ERR_INVALID_ARG),
+    (dict(seq_q=9), tb.TK_ERR_INVALID_ARG),                    # causal needs Sq <= Sk
+    (dict(seq_k=0, causal=0), tb.TK_ERR_INVALID_ARG),
+    (dict(dO=None), tb.TK_ERR_INVALID_ARG),
+    (dict(lse=None), tb.TK_ERR_INVALID_ARG),
+    (dict(dK=P_ODD), tb.TK_ERR_INVALID_ARG),
+    (dict(lse=ctypes.c_void_p(0x10002)), tb.TK_ERR_INVALID_ARG),
+    (dict(ws=None), tb.TK_ERR_WORKSPACE),
+    (dict(ws_bytes=16), tb.TK_ERR_WORKSPACE),
+    (dict(r=16), tb.TK_ERR_UNSUPPORTED),
+    (dict(d_v=96), tb.TK_ERR_UNSUPPORTED),
+    (dict(batch=0), tb.TK_OK),
+    (dict(seq_q=0, seq_k=0, Q=None, O=None, dO=None, lse=None, dQ=None), tb.TK_OK),
+])
+def test_backward_validation(kw, status):
+    assert backward(**kw) == status
+
+
+def test_backward_workspace_query():
+    ws = tb.tk_attn_prefill_backward_workspace_bytes
+    assert ws(4, 32, 8192) == 4 * 32 * 8192 * 4
+    assert ws(1, 3, 5) == 256
+    assert ws(0, 4, 10) == 256 and ws(1, 4, 0) == 256
+    assert ws(-1, 4, 10) == 0 and ws(1, 0, 10) == 0
+
+
 def decode(**kw):
     a = dict(Q=P, K=P, V=P, O=P, batch=2, H_q=32, H_kv=8, ctx_lens=P, max_ctx=4096, r=32, d_v=128,
              scale=0.0, k_dtype=tb.TK_BF16, k_scale=None, block_table=None, block_size=0,

@@ -129,3 +129,35 @@ def test_bf16_inputs_are_widened_exactly():
     b = oracle.prefill_backward(q.double(), k.double(), v.double(), do.double(), causal=True)
     for x, y in zip(a, b):
         assert torch.equal(x, y)
+
+
+def test_stored_output_enters_through_D_only():
+    """With O given, D = rowsum(dO * O). With the exact forward output this is the
+    default gradient; a perturbation Delta of O moves D_i by dO_i . Delta_i, which
+    leaves dV unchanged and moves dQ_i by -scale * (dO_i . Delta_i) * sum_j P_ij k_j and
+    dK_j by -scale * sum_i P_ij (dO_i . Delta_i) q_i (first order is exact: D enters
+    linearly)."""
+    B, Hq, Hkv, Sq, Sk, r, dv = 1, 4, 2, 9, 13, 4, 6
+    q, k, v = rand((B, Hq, Sq, r), 51), rand((B, Hkv, Sk, r), 52), rand((B, Hkv, Sk, dv), 53)
+    do = rand((B, Hq, Sq, dv), 54)
+    scale = 0.6
+    o = oracle.prefill(q, k, v, causal=True, scale=scale)
+    base = oracle.prefill_backward(q, k, v, do, causal=True, scale=scale)
+    same = oracle.prefill_backward(q, k, v, do, causal=True, scale=scale, o=o)
+    for x, y in zip(base, same):
+        assert (x - y).abs().max().item() <= 1e-12
+    delta = 1e-2 * rand((B, Hq, Sq, dv), 55)
+    moved = oracle.prefill_backward(q, k, v, do, causal=True, scale=scale, o=o + delta)
+    dD = (do * delta).sum(-1)                                    # [B, Hq, Sq]
+    G = Hq // Hkv
+    kr = k.repeat_interleave(G, dim=1)
+    s = (q @ kr.transpose(-1, -2)) * scale
+    i = torch.arange(Sq).view(-1, 1)
+    j = torch.arange(Sk).view(1, -1)
+    p = torch.softmax(s.masked_fill(j > i + (Sk - Sq), float("-inf")), dim=-1)
+    exp_dq = base[0] - scale * dD.unsqueeze(-1) * (p @ kr)
+    exp_dk = base[1] - scale * ((p * dD.unsqueeze(-1)).transpose(-1, -2) @ q).view(B, Hkv, G, Sk, r).sum(2)
+    assert (moved[0] - exp_dq).abs().max().item() <= 1e-12
+    assert (moved[1] - exp_dk).abs().max().item() <= 1e-12
+    assert (moved[2] - base[2]).abs().max().item() <= 1e-12
+    assert (moved[0] - base[0]).abs().max().item() > 1e-4      # the perturbation is visible

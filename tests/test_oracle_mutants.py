@@ -55,6 +55,7 @@ BACKWARD_MUTANTS = {
     "bwd_score_scale_dropped": ("s[j] = acc * scale;", "s[j] = acc;"),
     "bwd_dv_value_row": ("dvv[c] += p * ld(dO, do_dt, idx * dv + c);",
                          "dvv[c] += p * ld(V, v_dt, (size_t)kidx * dv + c);"),
+    "bwd_stored_o_ignored": ("            if (O) {\n                D = 0.0;", "            if (0) {\n                D = 0.0;"),
 }
 PIN_FILES = {**{n: "test_oracle_pins.py" for n in MUTANTS}, **{n: "test_oracle_backward.py" for n in BACKWARD_MUTANTS}}
 ALL_MUTANTS = {**MUTANTS, **BACKWARD_MUTANTS}
