@@ -21,6 +21,9 @@ The JSON line reports, besides the contract fields:
                 per (sequence, KV head) of the prefill shape with bf16, fp8 and
                 4-bit keys (quantised on write), and one decode token of the
                 batch-16 shape;
+  prefill_backward  the backward pass (dQ, dK, dV) of the 8192-token prefill,
+                thin keys and the full-key control, against the bf16 MFMA peak
+                with the algorithmic FLOPs 2 (3r + 2 d_v) per visible pair;
   fullkey_control  the batch-16 decode, the 8192-token prefill, the
                 131072-token paged decode and the 4-bit-key decode again with
                 standard-width bf16 keys (r = 128, same values), and the thin-key
@@ -44,6 +47,7 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.json")
 KERNEL_SOURCES = {"decode": "paper_2603_04427_amd/csrc/decode.hip",
                   "prefill_bf16": "paper_2603_04427_amd/csrc/prefill_bf16.hip",
                   "prefill_f32": "paper_2603_04427_amd/csrc/prefill_f32.hip",
+                  "prefill_bwd": "paper_2603_04427_amd/csrc/prefill_bwd.hip",
                   "append": "paper_2603_04427_amd/csrc/append.hip"}
 
 
@@ -166,6 +170,36 @@ def prefill_result(name, spec, dev, steps, warmup):
     }
 
 
+def backward_result(name, spec, dev, steps, warmup):
+    """tk_attn_prefill_backward (both kernels) on a prefill shape; the forward with
+    log-sum-exp runs once, untimed, to produce O and lse."""
+    import torch
+    from paper_2603_04427_amd import accounting as acc
+    from paper_2603_04427_amd import prepare_prefill_backward, tk_attn_prefill_lse
+    from synth import make_prefill, make_prefill_grad
+
+    p = make_prefill(spec, device=dev)
+    do = make_prefill_grad(spec, device=dev)
+    o, lse = tk_attn_prefill_lse(p["q"], p["k"], p["v"], causal=spec.causal, scale=spec.softmax_scale)
+    call = prepare_prefill_backward(p["q"], p["k"], p["v"], o, do, lse, causal=spec.causal,
+                                    scale=spec.softmax_scale)
+    wall, ev = time_calls([call], steps, warmup)
+    flops = acc.prefill_backward_flops(spec.batch, spec.h_q, spec.seq_q, spec.seq_k, spec.r, spec.d_v,
+                                       spec.causal)
+    peak = acc.BF16_MFMA_PEAK_TFLOPS
+    achieved = flops / ev / 1e12
+    del p, do, o, lse, call
+    torch.cuda.empty_cache()
+    return {
+        "workload": name, "value": round(flops / wall / 1e12, 2), "unit": "TFLOP/s",
+        "ms_per_call": round(wall * 1e3, 5), "dtype": spec.dtype,
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
+                     "frac": round(achieved / peak, 4), "traffic": traffic_for(name, "prefill_bwd"),
+                     "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5),
+                     "kernels": "bwd_dq_kernel + bwd_dkdv_kernel"},
+    }
+
+
 APPEND_CASES = {"cache_append_s8192": (4, 8192, "bf16"), "cache_append_fp8_s8192": (4, 8192, "fp8"),
                 "cache_append_int4_s8192": (4, 8192, "int4"), "cache_append_decode_b16": (16, 1, "bf16")}
 
@@ -269,6 +303,15 @@ def main():
                           "data": "synthetic", "config": {"workload": args.only}, "roofline": res["roofline"]}),
               flush=True)
         return
+    if args.only and args.only.endswith("_backward"):
+        spec = workloads[args.only[:-len("_backward")]]
+        res = backward_result(args.only, spec, dev, args.steps, min(args.warmup, 3))
+        print(json.dumps({"metric": "prefill backward TFLOP/s", "value": res["value"], "unit": "TFLOP/s",
+                          "n_gpus": 1, "steps": args.steps, "warmup": min(args.warmup, 3),
+                          "ms_per_step": res["ms_per_call"], "higher_is_better": True, "scaling": "weak",
+                          "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+                          "config": {"workload": args.only}, "roofline": res["roofline"]}), flush=True)
+        return
     main_name = args.only or "mistral_decode_b16"
     results = {}
     order = [main_name] if (args.no_secondary or args.only) else \
@@ -306,6 +349,17 @@ def main():
             full["thin_key_speedup"] = round(full["roofline"]["kernel_ms"] / thin["roofline"]["kernel_ms"], 3)
             full["ideal_speedup"] = round(ideal, 3)
             fullkey.append(full)
+    backward = []
+    if not (args.only or args.no_secondary):
+        for base in ("mistral_prefill_s8192", "mistral_prefill_s8192_fullkey"):
+            print(f"bench: timing {base}_backward", file=sys.stderr, flush=True)
+            backward.append(backward_result(base + "_backward", workloads[base], dev, max(5, args.steps // 20),
+                                            min(args.warmup, 3)))
+        if len(backward) == 2:
+            thin, full = backward
+            full["thin_key_speedup"] = round(full["roofline"]["kernel_ms"] / thin["roofline"]["kernel_ms"], 3)
+            tspec, fspec = workloads["mistral_prefill_s8192"], workloads["mistral_prefill_s8192_fullkey"]
+            full["ideal_speedup"] = round((3 * fspec.r + 2 * fspec.d_v) / (3 * tspec.r + 2 * tspec.d_v), 3)
     appends = []
     if not (args.only or args.no_secondary):
         for name, (B, T, kdt) in APPEND_CASES.items():
@@ -335,6 +389,8 @@ def main():
     line["secondary"] = [results[n] for n in order if n != main_name]
     if fullkey:
         line["fullkey_control"] = fullkey
+    if backward:
+        line["prefill_backward"] = backward
     if appends:
         line["cache_append"] = appends
     line["device"] = torch.cuda.get_device_name(0)

@@ -81,6 +81,16 @@ def prefill_flops(batch: int, h_q: int, seq_q: int, seq_k: int, r: int, d_v: int
     return batch * h_q * pairs * 2 * (r + d_v)
 
 
+def prefill_backward_flops(batch: int, h_q: int, seq_q: int, seq_k: int, r: int, d_v: int,
+                           causal: bool = True) -> int:
+    """Algorithmic FLOPs of the backward pass: per visible (query head, key) pair the
+    five products S = Q K^T (2r), dP = dO V^T (2 d_v), dV = P^T dO (2 d_v),
+    dQ = dS K (2r) and dK = dS^T Q (2r), so 2 (3r + 2 d_v). Work a kernel repeats
+    (recomputing S and dP in a second pass) is not counted."""
+    pairs = causal_pairs(seq_q, seq_k) if causal else seq_q * seq_k
+    return batch * h_q * pairs * 2 * (3 * r + 2 * d_v)
+
+
 def prefill_bytes(batch: int, h_q: int, h_kv: int, seq_q: int, seq_k: int, r: int, d_v: int,
                   elem_bytes: int) -> int:
     """Compulsory bytes of a prefill call: Q, K, V read once and O written once."""

@@ -181,6 +181,10 @@ def test_kernel_work_figures():
     c3 = WORKLOADS["mistral_prefill_s8192"]
     f = acc.prefill_flops(c3.batch, c3.h_q, c3.seq_q, c3.seq_k, c3.r, c3.d_v)
     assert f == 4 * 32 * (8192 * 8193 // 2) * 320
+    # backward: five products per visible pair, 3 of width r and 2 of width d_v
+    fb = acc.prefill_backward_flops(c3.batch, c3.h_q, c3.seq_q, c3.seq_k, c3.r, c3.d_v)
+    assert fb == 4 * 32 * (8192 * 8193 // 2) * 2 * (3 * 32 + 2 * 128)
+    assert acc.prefill_backward_flops(1, 1, 3, 3, 4, 8, causal=False) == 9 * 2 * (12 + 16)
     assert acc.causal_pairs(5, 8) == sum(min(8, i + 3 + 1) for i in range(5)) == 4 + 5 + 6 + 7 + 8
     c5 = WORKLOADS["fp8key_decode"]
     assert acc.decode_bytes(c5.lens, 32, 8, 32, 128, "fp8") == 32 * 8 * 32768 * 292 + 32 * 32 * 32 * 2 + 32 * 32 * 256 + 128
