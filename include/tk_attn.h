@@ -89,8 +89,9 @@ tk_status tk_attn_prefill_lse(const void* Q, const void* K, const void* V, void*
                               int causal, float scale, hipStream_t stream);
 
 /*
- * Bytes of device workspace tk_attn_prefill_backward needs: one fp32 per query
- * row (D = rowsum(dO * O)), rounded up to 256. Returns 0 for invalid shapes.
+ * Bytes of device workspace tk_attn_prefill_backward needs: two fp32 per query
+ * row (D = rowsum(dO * O) and the row's log-sum-exp in log2 units), rounded up
+ * to 256 (at least 256). Returns 0 for invalid shapes.
  */
 size_t tk_attn_prefill_backward_workspace_bytes(int batch, int H_q, int seq_q);
 

@@ -96,7 +96,7 @@ size_t tk_attn_prefill_backward_workspace_bytes(int batch, int H_q, int seq_q) {
     if (batch < 0 || H_q <= 0 || seq_q < 0) return 0;
     size_t rows = (size_t)batch * (size_t)H_q * (size_t)seq_q;
     rows = rows > 0 ? rows : 1;
-    return (rows * sizeof(float) + 255) / 256 * 256;
+    return (2 * rows * sizeof(float) + 255) / 256 * 256;
 }
 
 tk_status tk_attn_prefill_backward(const void* Q, const void* K, const void* V, const void* O, const void* dO,
@@ -133,6 +133,7 @@ tk_status tk_attn_prefill_backward(const void* Q, const void* K, const void* V, 
     p.dk = dK;
     p.dv = dV;
     p.delta = (float*)workspace;
+    p.lse2 = p.delta + (size_t)batch * H_q * seq_q;
     p.B = batch;
     p.Hq = H_q;
     p.Hkv = H_kv;

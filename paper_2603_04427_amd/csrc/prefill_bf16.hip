@@ -94,28 +94,6 @@ struct TileLanes {
     }
 };
 
-// Global->LDS copy of 16 bytes per lane (global_load_lds_dwordx4: lane i writes
-// LDS bytes lds + 16 i .. + 15 from base + off). It is issued as inline assembly
-// on purpose: for the compiler's own form of this copy, every later transposing
-// LDS read waits for all copies in flight, including the next tile's copy into
-// the other buffer, which would stall each tile halfway. The copies are awaited
-// explicitly (wait_loads) before the barrier that publishes a tile. M0, which
-// holds the LDS destination, is restored afterwards.
-__device__ __forceinline__ void copy16_to_lds(const char* base, uint32_t off, const uint16_t* lds) {
-    const uint32_t la = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds;
-    uint32_t saved;
-    asm volatile(
-        "s_mov_b32 %0, m0\n\t"
-        "s_mov_b32 m0, %3\n\t"
-        "s_nop 0\n\t"
-        "global_load_lds_dwordx4 %1, %2\n\t"
-        "s_nop 0\n\t"
-        "s_mov_b32 m0, %0"
-        : "=&s"(saved)
-        : "v"(off), "s"(base), "s"(la)
-        : "memory");
-}
-
 // Issue the copies of the tile starting at key `base` (wave `wave` copies its
 // 1 KB slices). A full tile needs no vector arithmetic: the global base and the
 // LDS destination are wave-uniform and the lane offsets are precomputed. Rows
@@ -155,9 +133,6 @@ __device__ __forceinline__ void load_tile(const TileLanes<R, DV, NT>& tl, uint16
         copy16_to_lds(vt, off, vs + (wave_base + i * NT) * 8);
     }
 }
-
-// All of this wave's vector memory operations (the tile copies) have completed.
-__device__ __forceinline__ void wait_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
 // exp2(s * c - m) for the 16 keys of k-step q of one 32-query block (accumulator
 // registers 8 (q % 2) .. + 7 of key block q / 2), rounded to a bf16 B operand of

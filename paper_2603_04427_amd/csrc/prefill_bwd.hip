@@ -100,30 +100,40 @@ __device__ __forceinline__ bf16x8 tr_operand(const uint16_t* tile, int r0, int c
     return a;
 }
 
-// Copies of a 64-row tile of width W: each thread moves CH 16-byte chunks,
-// global -> registers (issued early) -> LDS (after the tile in LDS is consumed).
-// Rows at or past `rows` repeat row rows - 1 (finite values, masked later).
+// This wave's share of the global->LDS copies of a 64-row tile of width W
+// (16-byte chunks; chunk i * 256 + 64 wave + lane of the tile for copy i of a
+// lane). LDS chunk (r, pos) receives global chunk (r, pos ^ swz(r)), which is the
+// swizzled layout the reads expect. Rows at or past `rows` re-read row rows - 1:
+// finite values, masked later.
 template <int W>
-struct TileStage {
+struct TileCopy {
     static constexpr int CHUNKS = kT * W / 8;
-    static constexpr int CH = (CHUNKS + kThreads - 1) / kThreads;
-    uint4 v[CH];
-    __device__ __forceinline__ void load(const uint16_t* g, int row0, int rows, int tid) {
-#pragma unroll
-        for (int i = 0; i < CH; ++i) {
-            const int c = tid + i * kThreads;
-            if (c < CHUNKS) {
-                int row = row0 + c / (W / 8);
-                row = row < rows ? row : rows - 1;
-                v[i] = *(const uint4*)(g + (size_t)row * W + (c % (W / 8)) * 8);
-            }
-        }
+    static constexpr int N = CHUNKS / kThreads;
+    static_assert(CHUNKS % kThreads == 0, "tile chunks must spread evenly over the workgroup");
+    // Copy i of a lane reads 256 chunks (4096 bytes) past copy i - 1: its row moves
+    // by a multiple of 16 (W = 128) or 32 (W = 64) rows, which leaves swz unchanged.
+    uint32_t off0;  // global byte offset (in the tile) of the lane's first chunk
+    int row0;       // its tile row
+    __device__ __forceinline__ TileCopy(int wave, int lane) {
+        const int ci = wave * 64 + lane;
+        const int r = ci / (W / 8), pos = ci % (W / 8);
+        row0 = r;
+        off0 = (uint32_t)((r * W + ((pos ^ swz<W>(r)) * 8)) * 2);
     }
-    __device__ __forceinline__ void store(uint16_t* tile, int tid) const {
+    __device__ __forceinline__ void issue(const uint16_t* g, int first, int rows, uint16_t* tile, int wave) const {
+        const char* t = (const char*)(g + (size_t)first * W);
+        if (first + kT <= rows) {  // workgroup-uniform
 #pragma unroll
-        for (int i = 0; i < CH; ++i) {
-            const int c = tid + i * kThreads;
-            if (c < CHUNKS) *(uint4*)((char*)tile + toff<W>(c / (W / 8), (c % (W / 8)) * 8)) = v[i];
+            for (int i = 0; i < N; ++i)
+                copy16_to_lds(t, off0 + i * kThreads * 16, tile + (i * kThreads + wave * 64) * 8);
+            return;
+        }
+        const int last = rows - first - 1;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            const int r = row0 + i * (kThreads * 8 / W);
+            const uint32_t o = off0 + i * kThreads * 16;
+            copy16_to_lds(t, r > last ? o - (r - last) * W * 2 : o, tile + (i * kThreads + wave * 64) * 8);
         }
     }
 };
@@ -142,15 +152,57 @@ __device__ __forceinline__ float bf16_at(const uint4& w, int e) {
     return (e & 1) ? bf16hi(x) : bf16lo(x);
 }
 
+// P = exp2(c S - lse2) and dS = P (dP - D) for the 16 rows 8 j + e (+ the lane's
+// 4 half) of a 32-row block, in place of S and dP. lq, dq: the block's lse2 and D
+// from the lane's first row. MASK: row u0 + 8 j + e counts only when it lies in
+// [0, span) (the rows that see the lane's key, relative to the first of them).
+template <bool MASK>
+__device__ __forceinline__ void kv_probs(f32x16& s, f32x16& dp, const float* lq, const float* dq, float c, int u0,
+                                         int span) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const float4 lj = *(const float4*)(lq + 8 * j);
+        const float4 dj = *(const float4*)(dq + 8 * j);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const int v = 4 * j + e;
+            const float l = e == 0 ? lj.x : e == 1 ? lj.y : e == 2 ? lj.z : lj.w;
+            const float dl = e == 0 ? dj.x : e == 1 ? dj.y : e == 2 ? dj.z : dj.w;
+            float x = exp2_fast(fmaf(s[v], c, -l));
+            if constexpr (MASK) x = (unsigned)(u0 + 8 * j + e) < (unsigned)span ? x : 0.f;
+            s[v] = x;
+            dp[v] = x * (dp[v] - dl);
+        }
+    }
+}
+
+// dS^T = P^T (dP^T - D) in place of S^T, P^T = exp2(c S^T - lse2), for the keys
+// 8 (v/4) + v % 4 (+ the lane's 4 half) of a 32-key block. MASK: keys past
+// `lim` (relative to the block's first key for this lane) weigh 0.
+template <bool MASK>
+__device__ __forceinline__ void q_dscores(f32x16& s, const f32x16& dp, float c, float lse2, float D, int lim) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+        float pr = exp2_fast(fmaf(s[v], c, -lse2));
+        if constexpr (MASK) pr = 8 * (v >> 2) + (v & 3) > lim ? 0.f : pr;
+        s[v] = pr * (dp[v] - D);
+    }
+}
+
 }  // namespace
 
 // ------------------------------------------------------------------ dQ and D
 
 template <int R, int DV>
+struct alignas(16) DqSmem {
+    uint16_t k[2][kT * R];
+    uint16_t v[2][kT * DV];
+};
+
+template <int R, int DV>
 __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(const PrefillBwdParams p, int n_groups) {
     constexpr int KSTEPS = R / 16, DSTEPS = DV / 16, RBLK = R / 32;
-    __shared__ __align__(16) uint16_t ks[kT * R];
-    __shared__ __align__(16) uint16_t vs[kT * DV];
+    __shared__ DqSmem<R, DV> sm;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int half = lane >> 5, col = lane & 31;
@@ -184,6 +236,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(const PrefillBwdPar
     const uint16_t* kg = (const uint16_t*)p.k + ((size_t)b * p.Hkv + g) * p.Sk * R;
     const uint16_t* vg = (const uint16_t*)p.v + ((size_t)b * p.Hkv + g) * p.Sk * DV;
 
+    const TileCopy<R> kc(wave, lane);
+    const TileCopy<DV> vc(wave, lane);
+    kc.issue(kg, 0, p.Sk, sm.k[0], wave);
+    vc.issue(vg, 0, p.Sk, sm.v[0], wave);
+
     // B operands: Q^T (dims 16m + 8 half .. + 7 of the lane's row) and dO^T; D from dO and O
     bf16x8 qreg[KSTEPS], dreg[DSTEPS];
 #pragma unroll
@@ -198,8 +255,11 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(const PrefillBwdPar
         for (int e = 0; e < 8; ++e) D = fmaf(bf16_at(dw, e), bf16_at(ow, e), D);
     }
     D = xor32_sum(D);
-    if (half == 0 && row_ok) p.delta[rowq * p.Sq + qrow] = D;
     const float lse2 = p.lse[rowq * p.Sq + qr] * kLog2e;
+    if (half == 0 && row_ok) {
+        p.delta[rowq * p.Sq + qrow] = D;
+        p.lse2[rowq * p.Sq + qrow] = lse2;
+    }
     const float c = p.qscale;
 
     int key_end = p.Sk;
@@ -217,54 +277,55 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(const PrefillBwdPar
 #pragma unroll
         for (int v = 0; v < 16; ++v) dq[rb][v] = 0.f;
 
-    TileStage<R> kst;
-    TileStage<DV> vst;
-    kst.load(kg, 0, p.Sk, tid);
-    vst.load(vg, 0, p.Sk, tid);
+    wait_loads();
+    // the same wait as a builtin, so that the compiler knows the row loads have
+    // landed and adds no wait of its own inside the tile loop (vmcnt 0)
+    __builtin_amdgcn_s_waitcnt(0x0F70);
+    __syncthreads();
+
     for (int t = 0; t < ntiles; ++t) {
+        const int cur = t & 1;
         const int base = t * kT;
-        __syncthreads();  // the previous tile has been consumed
-        kst.store(ks, tid);
-        vst.store(vs, tid);
-        __syncthreads();
         if (t + 1 < ntiles) {
-            kst.load(kg, base + kT, p.Sk, tid);
-            vst.load(vg, base + kT, p.Sk, tid);
+            kc.issue(kg, base + kT, p.Sk, sm.k[cur ^ 1], wave);
+            vc.issue(vg, base + kT, p.Sk, sm.v[cur ^ 1], wave);
         }
-        if (base > wave_last_key) continue;
-        const bool needs_mask = (p.causal && base + kT - 1 > qw0 + off) || base + kT > p.Sk;
+        if (base <= wave_last_key) {
+            const uint16_t* ks = sm.k[cur];
+            const uint16_t* vs = sm.v[cur];
+            const bool needs_mask = (p.causal && base + kT - 1 > qw0 + off) || base + kT > p.Sk;
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb) {
-            // S^T and dP^T of keys base + 32 kb + (8 (v/4) + 4 half + v % 4), query col
-            f32x16 s, dp;
+            for (int kb = 0; kb < 2; ++kb) {
+                // S^T and dP^T of keys base + 32 kb + (8 (v/4) + 4 half + v % 4), query col
+                f32x16 s, dp;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) s[v] = dp[v] = 0.f;
+                for (int v = 0; v < 16; ++v) s[v] = dp[v] = 0.f;
 #pragma unroll
-            for (int m = 0; m < KSTEPS; ++m)
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_operand<R>(ks, kb * 32 + col, 16 * m + 8 * half),
-                                                            qreg[m], s, 0, 0, 0);
+                for (int m = 0; m < KSTEPS; ++m)
+                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_operand<R>(ks, kb * 32 + col, 16 * m + 8 * half),
+                                                                qreg[m], s, 0, 0, 0);
 #pragma unroll
-            for (int m = 0; m < DSTEPS; ++m)
-                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_operand<DV>(vs, kb * 32 + col, 16 * m + 8 * half),
-                                                             dreg[m], dp, 0, 0, 0);
-            // dS^T = P^T (dP^T - D), P^T = exp2(c S^T - log2-domain L); masked keys weigh 0
+                for (int m = 0; m < DSTEPS; ++m)
+                    dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        row_operand<DV>(vs, kb * 32 + col, 16 * m + 8 * half), dreg[m], dp, 0, 0, 0);
+                // dS^T = P^T (dP^T - D), P^T = exp2(c S^T - log2-domain L); masked keys weigh 0
+                if (needs_mask)
+                    q_dscores<true>(s, dp, c, lse2, D, lim - (base + kb * 32 + 4 * half));
+                else
+                    q_dscores<false>(s, dp, c, lse2, D, 0);
+                // dQ^T += K^T dS^T over the block's two 16-key steps
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int key = base + kb * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-                float pr = exp2_fast(fmaf(s[v], c, -lse2));
-                if (needs_mask && key > lim) pr = 0.f;
-                s[v] = pr * (dp[v] - D);
-            }
-            // dQ^T += K^T dS^T over the block's two 16-key steps
+                for (int sub = 0; sub < 2; ++sub) {
+                    const bf16x8 bop = pack_step(s, sub);
 #pragma unroll
-            for (int sub = 0; sub < 2; ++sub) {
-                const bf16x8 bop = pack_step(s, sub);
-#pragma unroll
-                for (int rb = 0; rb < RBLK; ++rb)
-                    dq[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                        tr_operand<R>(ks, kb * 32 + 16 * sub, 32 * rb, lane), bop, dq[rb], 0, 0, 0);
+                    for (int rb = 0; rb < RBLK; ++rb)
+                        dq[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                            tr_operand<R>(ks, kb * 32 + 16 * sub, 32 * rb, lane), bop, dq[rb], 0, 0, 0);
+                }
             }
         }
+        if (t + 1 < ntiles) wait_loads();  // this wave's part of the next tile has landed
+        __syncthreads();
     }
 
     // dQ rows: lane (half, col) holds dims 32 rb + 8 (v/4) + 4 half + v % 4 of row qrow
@@ -284,15 +345,42 @@ __global__ __launch_bounds__(kThreads, 2) void bwd_dq_kernel(const PrefillBwdPar
 
 // ------------------------------------------------------------------ dK and dV
 
-// Register budget: the dK and dV accumulators (r + d_v per lane), the K and V
-// rows and the staged tiles fit two workgroups per CU while r + d_v < 192.
 template <int R, int DV>
-__global__ __launch_bounds__(kThreads, R + DV >= 192 ? 1 : 2) void bwd_dkdv_kernel(const PrefillBwdParams p, int n_groups) {
+struct alignas(16) KvSmem {
+    uint16_t q[2][kT * R];
+    uint16_t d[2][kT * DV];
+    float lse2[2][kT];  // log2-domain log-sum-exp of the tile's rows
+    float dl[2][kT];    // D of the tile's rows
+};
+
+// Issue the copies of query tile `it` (head g G + it / n_rt, rows from
+// (t0 + it % n_rt) 64) into buffer `buf`: Q and dO rows by all waves, the rows'
+// lse2 by wave 0 and D by wave 1 (one float per lane, rows clamped to Sq - 1).
+template <int R, int DV>
+__device__ __forceinline__ void issue_qtile(const PrefillBwdParams& p, KvSmem<R, DV>& sm, const TileCopy<R>& qc,
+                                            const TileCopy<DV>& dc, int it, int buf, int b, int g, int t0,
+                                            int n_rt, int wave, int lane) {
+    const int hh = g * p.G + it / n_rt;
+    const int row0 = (t0 + it % n_rt) * kT;
+    const size_t rowq = (size_t)b * p.Hq + hh;
+    qc.issue((const uint16_t*)p.q + rowq * p.Sq * R, row0, p.Sq, sm.q[buf], wave);
+    dc.issue((const uint16_t*)p.dout + rowq * p.Sq * DV, row0, p.Sq, sm.d[buf], wave);
+    if (wave < 2) {
+        int r = row0 + lane;
+        r = r < p.Sq ? r : p.Sq - 1;
+        const float* src = wave == 0 ? p.lse2 : p.delta;
+        copy4_to_lds((const char*)(src + rowq * p.Sq), (uint32_t)r * 4u, wave == 0 ? sm.lse2[buf] : sm.dl[buf]);
+    }
+}
+
+// Register budget: the dK and dV accumulators (r + d_v per lane) and the K and V
+// rows fit two workgroups per CU while r + d_v < 192.
+template <int R, int DV>
+__global__ __launch_bounds__(kThreads, R + DV >= 192 ? 1 : 2) void bwd_dkdv_kernel(const PrefillBwdParams p,
+                                                                                    int n_groups) {
     constexpr int KSTEPS = R / 16, DSTEPS = DV / 16, RBLK = R / 32, DBLK = DV / 32;
     constexpr int KB = 4 * 32;  // keys per workgroup
-    __shared__ __align__(16) uint16_t qs[kT * R];
-    __shared__ __align__(16) uint16_t ds[kT * DV];
-    __shared__ float lse_s[kT], d_s[kT];
+    __shared__ KvSmem<R, DV> sm;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int half = lane >> 5, col = lane & 31;
@@ -309,10 +397,25 @@ __global__ __launch_bounds__(kThreads, R + DV >= 192 ? 1 : 2) void bwd_dkdv_kern
     const int key = k0 + col;              // this lane's key (B-operand column)
     const bool key_ok = key < p.Sk;
     const int off = p.Sk - p.Sq;
+    // rows that see this lane's key: [rmin, rmin + span)
+    const int rmin = p.causal ? key - off : 0;
+    const int span = key_ok ? p.Sq - rmin : 0;  // >= 1: key - off <= Sq - 1
 
     const size_t kvrow = (size_t)b * p.Hkv + g;
     const uint16_t* kg = (const uint16_t*)p.k + kvrow * p.Sk * R;
     const uint16_t* vg = (const uint16_t*)p.v + kvrow * p.Sk * DV;
+
+    // query tiles that see any key of the workgroup
+    int first_row = p.causal ? k0g - off : 0;
+    first_row = first_row < 0 ? 0 : first_row;
+    const int t0 = first_row / kT;
+    const int nt = (p.Sq + kT - 1) / kT;
+    const int n_rt = nt - t0;
+    const int n_iter = n_rt * p.G;  // (head, tile) pairs
+
+    const TileCopy<R> qc(wave, lane);
+    const TileCopy<DV> dc(wave, lane);
+    if (n_iter > 0) issue_qtile<R, DV>(p, sm, qc, dc, 0, 0, b, g, t0, n_rt, wave, lane);
 
     // B operands of S = Q K^T and dP = dO V^T: the lane's key row
     bf16x8 kreg[KSTEPS], vreg[DSTEPS];
@@ -338,81 +441,58 @@ __global__ __launch_bounds__(kThreads, R + DV >= 192 ? 1 : 2) void bwd_dkdv_kern
 #pragma unroll
         for (int v = 0; v < 16; ++v) dka[rb][v] = 0.f;
 
-    // query tiles that see any key of the workgroup
-    int first_row = p.causal ? k0g - off : 0;
-    first_row = first_row < 0 ? 0 : first_row;
-    const int t0 = first_row / kT;
-    const int nt = (p.Sq + kT - 1) / kT;
-    const int n_iter = (nt - t0) * p.G;  // (head, tile) pairs
+    wait_loads();
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt 0, known to the compiler
+    __syncthreads();
 
-    TileStage<R> qst;
-    TileStage<DV> dst;
-    float lse_v = 0.f, d_v = 0.f;
-    auto stage = [&](int it) {
-        const int hh = g * p.G + it / (nt - t0);
-        const int row0 = (t0 + it % (nt - t0)) * kT;
-        const size_t rowq = (size_t)b * p.Hq + hh;
-        qst.load((const uint16_t*)p.q + rowq * p.Sq * R, row0, p.Sq, tid);
-        dst.load((const uint16_t*)p.dout + rowq * p.Sq * DV, row0, p.Sq, tid);
-        int r = row0 + (tid & (kT - 1));
-        r = r < p.Sq ? r : p.Sq - 1;
-        if (tid < kT) lse_v = p.lse[rowq * p.Sq + r] * kLog2e;
-        else if (tid < 2 * kT) d_v = p.delta[rowq * p.Sq + r];
-    };
-    if (n_iter > 0) stage(0);
     for (int it = 0; it < n_iter; ++it) {
-        const int i0 = (t0 + it % (nt - t0)) * kT;  // first query row of the tile
-        __syncthreads();  // the previous tile has been consumed
-        qst.store(qs, tid);
-        dst.store(ds, tid);
-        if (tid < kT) lse_s[tid] = lse_v;
-        else if (tid < 2 * kT) d_s[tid - kT] = d_v;
-        __syncthreads();
-        if (it + 1 < n_iter) stage(it + 1);
-        if (p.causal && i0 + kT - 1 + off < k0) continue;  // no row of the tile sees the wave's keys
-        const bool needs_mask = (p.causal && i0 + off < k0 + 31) || i0 + kT > p.Sq || k0 + 32 > p.Sk;
+        const int cur = it & 1;
+        const int i0 = (t0 + it % n_rt) * kT;  // first query row of the tile
+        if (it + 1 < n_iter) issue_qtile<R, DV>(p, sm, qc, dc, it + 1, cur ^ 1, b, g, t0, n_rt, wave, lane);
+        if (!(p.causal && i0 + kT - 1 + off < k0)) {  // some row of the tile sees the wave's keys
+            const uint16_t* qs = sm.q[cur];
+            const uint16_t* ds = sm.d[cur];
+            const bool needs_mask = (p.causal && i0 + off < k0 + 31) || i0 + kT > p.Sq || k0 + 32 > p.Sk;
 #pragma unroll
-        for (int qb = 0; qb < 2; ++qb) {
-            // S and dP of query rows i0 + 32 qb + (8 (v/4) + 4 half + v % 4), key col
-            f32x16 s, dp;
+            for (int qb = 0; qb < 2; ++qb) {
+                // S and dP of query rows i0 + 32 qb + (8 (v/4) + 4 half + v % 4), key col
+                f32x16 s, dp;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) s[v] = dp[v] = 0.f;
+                for (int v = 0; v < 16; ++v) s[v] = dp[v] = 0.f;
 #pragma unroll
-            for (int m = 0; m < KSTEPS; ++m)
-                s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_operand<R>(qs, qb * 32 + col, 16 * m + 8 * half),
-                                                            kreg[m], s, 0, 0, 0);
+                for (int m = 0; m < KSTEPS; ++m)
+                    s = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_operand<R>(qs, qb * 32 + col, 16 * m + 8 * half),
+                                                                kreg[m], s, 0, 0, 0);
 #pragma unroll
-            for (int m = 0; m < DSTEPS; ++m)
-                dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(row_operand<DV>(ds, qb * 32 + col, 16 * m + 8 * half),
-                                                             vreg[m], dp, 0, 0, 0);
-            f32x16 pr;
+                for (int m = 0; m < DSTEPS; ++m)
+                    dp = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                        row_operand<DV>(ds, qb * 32 + col, 16 * m + 8 * half), vreg[m], dp, 0, 0, 0);
+                // P and dS = P (dP - D) replace S and dP in place; masked pairs weigh 0
+                const float* lq = &sm.lse2[cur][qb * 32 + 4 * half];
+                const float* dq = &sm.dl[cur][qb * 32 + 4 * half];
+                if (needs_mask)
+                    kv_probs<true>(s, dp, lq, dq, c, i0 + qb * 32 + 4 * half - rmin, span);
+                else
+                    kv_probs<false>(s, dp, lq, dq, c, 0, 0);
+                // dV += P^T dO and dK += dS^T Q over the block's two 16-row steps
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int lr = qb * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-                float x = exp2_fast(fmaf(s[v], c, -lse_s[lr]));
-                if (needs_mask) {
-                    const int row = i0 + lr;
-                    if (row >= p.Sq || !key_ok || (p.causal && key > row + off)) x = 0.f;
+                for (int sub = 0; sub < 2; ++sub) {
+                    const bf16x8 pa = pack_step(s, sub);
+                    const bf16x8 sa = pack_step(dp, sub);
+                    const int r0 = qb * 32 + 16 * sub;
+#pragma unroll
+                    for (int d = 0; d < DBLK; ++d)
+                        dva[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, tr_operand<DV>(ds, r0, 32 * d, lane),
+                                                                         dva[d], 0, 0, 0);
+#pragma unroll
+                    for (int rb = 0; rb < RBLK; ++rb)
+                        dka[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa, tr_operand<R>(qs, r0, 32 * rb, lane),
+                                                                          dka[rb], 0, 0, 0);
                 }
-                pr[v] = x;
-                s[v] = x * (dp[v] - d_s[lr]);  // dS
-            }
-            // dV += P^T dO and dK += dS^T Q over the block's two 16-row steps
-#pragma unroll
-            for (int sub = 0; sub < 2; ++sub) {
-                const bf16x8 pa = pack_step(pr, sub);
-                const bf16x8 sa = pack_step(s, sub);
-                const int r0 = qb * 32 + 16 * sub;
-#pragma unroll
-                for (int d = 0; d < DBLK; ++d)
-                    dva[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(pa, tr_operand<DV>(ds, r0, 32 * d, lane), dva[d],
-                                                                     0, 0, 0);
-#pragma unroll
-                for (int rb = 0; rb < RBLK; ++rb)
-                    dka[rb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(sa, tr_operand<R>(qs, r0, 32 * rb, lane),
-                                                                      dka[rb], 0, 0, 0);
             }
         }
+        if (it + 1 < n_iter) wait_loads();  // this wave's part of the next tile has landed
+        __syncthreads();
     }
 
     // dK, dV rows: lane (half, col) holds keys k0 + 8 (v/4) + 4 half + v % 4, column col of each block

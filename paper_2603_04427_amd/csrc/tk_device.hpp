@@ -153,4 +153,46 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// Global->LDS copy of 16 bytes per lane (global_load_lds_dwordx4: lane i writes
+// LDS bytes lds + 16 i .. + 15 from base + off). It is issued as inline assembly
+// on purpose: for the compiler's own form of this copy, every later transposing
+// LDS read waits for all copies in flight, including the next tile's copy into
+// the other buffer, which would stall each tile halfway. The copies are awaited
+// explicitly (wait_loads) before the barrier that publishes a tile. M0, which
+// holds the LDS destination, is restored afterwards.
+__device__ __forceinline__ void copy16_to_lds(const char* base, uint32_t off, const uint16_t* lds) {
+    const uint32_t la = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds;
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, %2\n\t"
+        "s_nop 0\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(off), "s"(base), "s"(la)
+        : "memory");
+}
+
+// Global->LDS copy of 4 bytes per lane (global_load_lds_dword: lane i writes LDS
+// bytes lds + 4 i .. + 3 from base + off), issued and awaited like copy16_to_lds.
+__device__ __forceinline__ void copy4_to_lds(const char* base, uint32_t off, const void* lds) {
+    const uint32_t la = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void*)lds;
+    uint32_t saved;
+    asm volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %3\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dword %1, %2\n\t"
+        "s_nop 0\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(off), "s"(base), "s"(la)
+        : "memory");
+}
+
+// All of this wave's vector memory operations (the tile copies) have completed.
+__device__ __forceinline__ void wait_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 }  // namespace tk

@@ -87,6 +87,7 @@ struct PrefillBwdParams {
     void* dk;           // [B, Hkv, Sk, R]
     void* dv;           // [B, Hkv, Sk, DV]
     float* delta;       // [B, Hq, Sq] workspace: D of each row
+    float* lse2;        // [B, Hq, Sq] workspace: the rows' log-sum-exp in log2 units
     int B, Hq, Hkv, G, Sq, Sk;
     int causal;
     float scale;        // softmax scale

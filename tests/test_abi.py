@@ -109,7 +109,7 @@ def test_backward_validation(kw, status):
 
 def test_backward_workspace_query():
     ws = tb.tk_attn_prefill_backward_workspace_bytes
-    assert ws(4, 32, 8192) == 4 * 32 * 8192 * 4
+    assert ws(4, 32, 8192) == 4 * 32 * 8192 * 8
     assert ws(1, 3, 5) == 256
     assert ws(0, 4, 10) == 256 and ws(1, 4, 0) == 256
     assert ws(-1, 4, 10) == 0 and ws(1, 0, 10) == 0
