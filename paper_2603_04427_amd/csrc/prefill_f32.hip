@@ -156,11 +156,17 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillP
     const int lane = tid & 63, wave = tid >> 6;
     const int half = lane >> 5, col = lane & 31;
 
+    // workgroup -> (query block, head, sequence): ranked by causal prefix length,
+    // longest first, with the heads and sequences of one rank adjacent, so that the
+    // round-robin dispatch over the XCDs deals every XCD the same mix of long and
+    // short blocks
     const int nqb = (p.Sq + kRows - 1) / kRows;
-    const int qb = p.causal ? nqb - 1 - (int)blockIdx.x : (int)blockIdx.x;  // longest prefixes first
-    const int h = blockIdx.y;
+    const int rank = (int)(blockIdx.x / ((unsigned)p.Hq * p.B));
+    const int hb = (int)(blockIdx.x % ((unsigned)p.Hq * p.B));
+    const int qb = p.causal ? nqb - 1 - rank : rank;
+    const int h = hb % p.Hq;
     const int g = h / p.G;
-    const int b = blockIdx.z;
+    const int b = hb / p.Hq;
     const int q0 = qb * kRows;
     const int off = p.Sk - p.Sq;  // bottom-right causal alignment
 
@@ -310,8 +316,9 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillP
 
 template <int R, int DV>
 static hipError_t run(const PrefillParams& p, hipStream_t st) {
-    if (p.Hq > 65535 || p.B > 65535) return hipErrorInvalidValue;
-    dim3 grid((p.Sq + kRows - 1) / kRows, p.Hq, p.B);
+    const long n = (long)((p.Sq + kRows - 1) / kRows) * p.Hq * p.B;
+    if (n > 0x7fffffffL) return hipErrorInvalidValue;
+    dim3 grid((unsigned)n);
     hipLaunchKernelGGL((prefill_f32_kernel<R, DV>), grid, dim3(kThreads), 0, st, p);
     return hipGetLastError();
 }
