@@ -24,6 +24,9 @@ The JSON line reports, besides the contract fields:
   prefill_backward  the backward pass (dQ, dK, dV) of the 8192-token prefill,
                 thin keys and the full-key control, against the bf16 MFMA peak
                 with the algorithmic FLOPs 2 (3r + 2 d_v) per visible pair;
+  device        the part's CU count, architecture and engine clock levels, and
+                the rates of torch's sum over 2 GiB and copy of 1 GiB on it
+                (context for the fractions of the published peaks);
   fullkey_control  the batch-16 decode, the 8192-token prefill, the
                 131072-token paged decode and the 4-bit-key decode again with
                 standard-width bf16 keys (r = 128, same values), and the thin-key
@@ -277,6 +280,52 @@ def copy_calibration(mib: int, dev):
     print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n, "launches": 3}))
 
 
+def device_context(dev):
+    """What the part reports and plain streaming rates measured on it, as context
+    for the roofline fractions (which use the published peaks): CU count and
+    architecture, the engine clock levels the driver lists, and the rates of
+    torch's own kernels for a read-only sum over 2 GiB and a 1 GiB copy (best of
+    5, HIP events). These are library kernels, not the part's ceiling."""
+    import glob
+    import torch
+    props = torch.cuda.get_device_properties(dev)
+    ctx = {"name": props.name, "arch": props.gcnArchName, "cus": props.multi_processor_count,
+           "sclk_mhz_levels": None, "torch_sum_read_GBps": None, "torch_copy_GBps": None}
+    for path in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
+        try:
+            with open(path) as f:
+                levels = [int(t.rstrip("*").lower().replace("mhz", ""))
+                          for line in f for t in line.split()[1:2] if t.lower().rstrip("*").endswith("mhz")]
+            if levels:
+                ctx["sclk_mhz_levels"] = levels
+                break
+        except (OSError, ValueError):
+            continue
+
+    def best(fn, nbytes):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        fn()
+        torch.cuda.synchronize()
+        t = []
+        for _ in range(5):
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            t.append(e0.elapsed_time(e1) / 1e3)
+        return round(nbytes / min(t) / 1e9, 1)
+
+    x = torch.ones((2 << 30) // 4, dtype=torch.float32, device=dev)
+    ctx["torch_sum_read_GBps"] = best(lambda: x.sum(), x.numel() * 4)
+    del x
+    src = torch.ones((1 << 30) // 4, dtype=torch.int32, device=dev)
+    dst = torch.empty_like(src)
+    ctx["torch_copy_GBps"] = best(lambda: dst.copy_(src), 2 * src.numel() * 4)
+    del src, dst
+    torch.cuda.empty_cache()
+    return ctx
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -393,7 +442,7 @@ def main():
         line["prefill_backward"] = backward
     if appends:
         line["cache_append"] = appends
-    line["device"] = torch.cuda.get_device_name(0)
+    line["device"] = device_context(dev)
     print(json.dumps(line), flush=True)
 
 
