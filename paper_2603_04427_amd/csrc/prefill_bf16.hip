@@ -23,7 +23,11 @@
 //    tile through the transposing LDS read ds_read_b64_tr_b16.
 //  * Online softmax in the log2 domain (scale * log2(e) applied by one FMA),
 //    with a lazy per-row rescale: a row's reference maximum moves only when its
-//    maximum exceeds it by more than 8 (a factor of 256).
+//    maximum exceeds it by more than 8 (a factor of 256). With one query block
+//    per wave the row sums run on the matrix core, which the vector softmax
+//    leaves idle about half the time: a 16x16x32 product of a 0/1 selector with
+//    each bf16 P^T operand adds up exactly the rounded probabilities that feed
+//    the value product, in place of 16 vector dot products per tile.
 //  * Causal masking only on tiles that cross a wave's diagonal; tiles above it
 //    are skipped. Workgroups are ordered so that the query blocks of one KV
 //    sequence run together on one XCD (its K/V stays in that XCD's L2),
@@ -73,25 +77,27 @@ struct TileLanes {
     static constexpr int VC = kBN * DV / 8;  // ... and in the V tile
     static constexpr int KL = (KC + NT - 1) / NT;
     static constexpr int VL = (VC + NT - 1) / NT;
-    uint32_t k_row[KL], k_off[KL];  // tile row and byte offset (in the tile) of each K chunk this lane copies
-    uint32_t v_row[VL], v_off[VL];
+    uint32_t k_off[KL];  // byte offset (in the tile) of each K chunk this lane copies
+    uint32_t v_off[VL];
+    int tid_;
 
-    __device__ __forceinline__ explicit TileLanes(int tid) {
+    __device__ __forceinline__ explicit TileLanes(int tid) : tid_(tid) {
 #pragma unroll
         for (int i = 0; i < KL; ++i) {
             const int ci = tid + i * NT;
             const int r = ci / (R / 8), pos = ci % (R / 8);
-            k_row[i] = r;
             k_off[i] = (uint32_t)((r * R + (pos ^ swz<R, false>(r)) * 8) * 2);
         }
 #pragma unroll
         for (int i = 0; i < VL; ++i) {
             const int ci = tid + i * NT;
             const int r = ci / (DV / 8), pos = ci % (DV / 8);
-            v_row[i] = r;
             v_off[i] = (uint32_t)((r * DV + (pos ^ swz<DV, true>(r)) * 8) * 2);
         }
     }
+    // tile rows of the chunks, recomputed (needed only for a ragged last tile)
+    __device__ __forceinline__ int k_row(int i) const { return (tid_ + i * NT) / (R / 8); }
+    __device__ __forceinline__ int v_row(int i) const { return (tid_ + i * NT) / (DV / 8); }
 };
 
 // Issue the copies of the tile starting at key `base` (wave `wave` copies its
@@ -123,13 +129,15 @@ __device__ __forceinline__ void load_tile(const TileLanes<R, DV, NT>& tl, uint16
 #pragma unroll
     for (int i = 0; i < T::KL; ++i) {
         if (T::KC % NT != 0 && wave_base + i * NT >= T::KC) break;
-        const uint32_t off = (int)tl.k_row[i] > last ? tl.k_off[i] - (tl.k_row[i] - last) * R * 2 : tl.k_off[i];
+        const int kr = tl.k_row(i);
+        const uint32_t off = kr > last ? tl.k_off[i] - (kr - last) * R * 2 : tl.k_off[i];
         copy16_to_lds(kt, off, ks + (wave_base + i * NT) * 8);
     }
 #pragma unroll
     for (int i = 0; i < T::VL; ++i) {
         if (T::VC % NT != 0 && wave_base + i * NT >= T::VC) break;
-        const uint32_t off = (int)tl.v_row[i] > last ? tl.v_off[i] - (tl.v_row[i] - last) * DV * 2 : tl.v_off[i];
+        const int vr = tl.v_row(i);
+        const uint32_t off = vr > last ? tl.v_off[i] - (vr - last) * DV * 2 : tl.v_off[i];
         copy16_to_lds(vt, off, vs + (wave_base + i * NT) * 8);
     }
 }
@@ -137,6 +145,7 @@ __device__ __forceinline__ void load_tile(const TileLanes<R, DV, NT>& tl, uint16
 // exp2(s * c - m) for the 16 keys of k-step q of one 32-query block (accumulator
 // registers 8 (q % 2) .. + 7 of key block q / 2), rounded to a bf16 B operand of
 // O^T = V^T P^T; the row-sum share accumulates the same rounded values.
+template <bool SUM = true>
 __device__ __forceinline__ bf16x8 prob_step(const f32x16 (&s)[2], int q, float m, float c, float& lsum) {
     uint32_t w[4];
 #pragma unroll
@@ -144,7 +153,7 @@ __device__ __forceinline__ bf16x8 prob_step(const f32x16 (&s)[2], int q, float m
         const float p0 = exp2_fast(fmaf(s[q >> 1][8 * (q & 1) + 2 * i], c, -m));
         const float p1 = exp2_fast(fmaf(s[q >> 1][8 * (q & 1) + 2 * i + 1], c, -m));
         w[i] = pack_bf16(p0, p1);
-        lsum = add_bf16_pair(w[i], lsum);
+        if constexpr (SUM) lsum = add_bf16_pair(w[i], lsum);
     }
     return __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
 }
@@ -181,7 +190,7 @@ __device__ __forceinline__ bf16x8 vt_operand(const uint16_t* vs, uint32_t vbase,
 
 // QC: 32-query column blocks per wave (1 or 2); NW: waves per workgroup.
 template <int R, int DV, int QC, int NW>
-__global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_kernel(const PrefillParams p,
+__global__ __launch_bounds__(64 * NW, QC == 1 ? (R <= 32 ? 3 : 2) : 1) void prefill_bf16_kernel(const PrefillParams p,
                                                                                      int n_groups) {
     constexpr int KSTEPS = R / 16;  // MFMA K-steps of the score product
     constexpr int DBLK = DV / 32;   // 32-row blocks of O^T
@@ -253,6 +262,19 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_ke
         lsum[qc] = 0.f;
     }
     const float c = p.qscale;
+    // Row sums on the matrix core (one query block per wave): a 16x16x32 product
+    // of a 0/1 selector with each P^T operand. Lanes 0 and 32 of the selector
+    // pick the keys a query's two lane halves hold into row 0 (query n), lanes 17
+    // and 49 into row 1 (query n + 16); lanes 0..15 of the accumulator then hold
+    // the sums of queries n (register 0) and n + 16 (register 1).
+    constexpr bool MSUM = QC == 1;
+    typedef float f32x4 __attribute__((ext_vector_type(4)));
+    f32x4 lacc = {0.f, 0.f, 0.f, 0.f};
+    bf16x8 sel;
+    {
+        const uint32_t one = (lane == 0 || lane == 32 || lane == 17 || lane == 49) ? 0x3F803F80u : 0u;
+        sel = __builtin_bit_cast(bf16x8, make_uint4(one, one, one, one));
+    }
 
     // Lane byte offsets of the LDS operands. The row swizzles reduce to lane
     // constants here: for K rows kb*32 + col the swizzle term depends on col
@@ -338,6 +360,11 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_ke
                     const float alpha = need ? exp2_fast(m_ref[qc] - mx2) : 1.f;
                     m_ref[qc] = need ? mx2 : m_ref[qc];
                     lsum[qc] *= alpha;
+                    if constexpr (MSUM) {
+                        const float alpha_hi = __shfl_xor(alpha, 16);  // query n + 16's factor
+                        lacc[0] *= alpha;
+                        lacc[1] *= alpha_hi;
+                    }
 #pragma unroll
                     for (int d = 0; d < DBLK; ++d)
 #pragma unroll
@@ -352,7 +379,7 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_ke
             bf16x8 va[DBLK];
 #pragma unroll
             for (int d = 0; d < DBLK; ++d) va[d] = vt_operand<DV>(vs, vaddr[d], 0);
-            bf16x8 p0 = prob_step(s[0], 0, m_ref[0], c, lsum[0]);
+            bf16x8 p0 = prob_step<!MSUM>(s[0], 0, m_ref[0], c, lsum[0]);
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 __builtin_amdgcn_sched_barrier(0);
@@ -364,10 +391,11 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_ke
                 bf16x8 p1 = p0;
                 if constexpr (QC == 2) p1 = prob_step(s[QC - 1], q, m_ref[QC - 1], c, lsum[QC - 1]);
                 bf16x8 p0n = p0;
-                if (q < 3) p0n = prob_step(s[0], q + 1, m_ref[0], c, lsum[0]);
+                if (q < 3) p0n = prob_step<!MSUM>(s[0], q + 1, m_ref[0], c, lsum[0]);
 #pragma unroll
                 for (int d = 0; d < DBLK; ++d)
                     o[0][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[d], p0, o[0][d], 0, 0, 0);
+                if constexpr (MSUM) lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(sel, p0, lacc, 0, 0, 0);
                 if constexpr (QC == 2) {
 #pragma unroll
                     for (int d = 0; d < DBLK; ++d)
@@ -376,9 +404,9 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_ke
                 // schedule: operand reads first, then one MFMA per few vector ops
                 __builtin_amdgcn_sched_group_barrier(0x100, 4 * DBLK, 0);
 #pragma unroll
-                for (int i = 0; i < QC * DBLK; ++i) {
+                for (int i = 0; i < QC * DBLK + (MSUM ? 1 : 0); ++i) {
                     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-                    __builtin_amdgcn_sched_group_barrier(0x402, 6, 0);
+                    __builtin_amdgcn_sched_group_barrier(0x402, MSUM ? 4 : 6, 0);
                 }
                 if (q < 3) {
                     p0 = p0n;
@@ -396,7 +424,14 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? 8 / NW : 1) void prefill_bf16_ke
     // log-sum-exp: the reference maximum plus log2 of the sum, in natural log)
 #pragma unroll
     for (int qc = 0; qc < QC; ++qc) {
-        const float ltot = xor32_sum(lsum[qc]);
+        float ltot;
+        if constexpr (MSUM) {
+            const float a0 = __shfl(lacc[0], col & 15);
+            const float a1 = __shfl(lacc[1], col & 15);
+            ltot = col < 16 ? a0 : a1;
+        } else {
+            ltot = xor32_sum(lsum[qc]);
+        }
         const float inv = 1.f / ltot;
         const int qrow = qw0 + 32 * qc + col;
         if (p.lse != nullptr && half == 0 && qrow < p.Sq)
