@@ -268,7 +268,6 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? (R <= 32 ? 3 : 2) : 1) void pref
     // and 49 into row 1 (query n + 16); lanes 0..15 of the accumulator then hold
     // the sums of queries n (register 0) and n + 16 (register 1).
     constexpr bool MSUM = QC == 1;
-    typedef float f32x4 __attribute__((ext_vector_type(4)));
     f32x4 lacc = {0.f, 0.f, 0.f, 0.f};
     bf16x8 sel;
     {

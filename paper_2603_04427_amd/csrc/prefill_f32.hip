@@ -1,26 +1,30 @@
 // Thin-key prefill attention for gfx950 with fp32 inputs and fp32 matrix cores
-// (v_mfma_f32_32x32x2f32), for callers that need fp32 accuracy (bf16 operands
+// (v_mfma_f32_16x16x4_f32), for callers that need fp32 accuracy (bf16 operands
 // would not hold a 1e-4 error bound).
 //
-// Work decomposition. The fp32 matrix instruction does 4096 FLOPs in 64 cycles,
-// so a 32-row query block against a long causal prefix is a long serial chain.
-// A workgroup therefore holds ONE block of 32 query rows of one head, and its 4
-// waves split that block's key tiles among themselves (wave w takes tiles w,
-// w + 4, ...), each wave with its own tile in LDS and its own online-softmax
+// Work decomposition. The fp32 matrix instructions are slow (64 FLOPs per cycle
+// per SIMD), so a causal prefill is bound by its longest query block, whose
+// whole key prefix runs on one CU. A workgroup therefore holds ONE block of 16
+// query rows of one head (half the matrix work of a 32-row block per key), and
+// its 4 waves split that block's key tiles among themselves (wave w takes tiles
+// w, w + 4, ...), each wave with its own tile in LDS and its own online-softmax
 // state; the 4 partial results are merged in LDS with the log-sum-exp rule at
-// the end. The longest chain is a quarter of the block's tiles, and a prefill
-// has one workgroup per (32 query rows, head).
+// the end. Workgroups are ranked by prefix length across heads and sequences,
+// longest first, so the round-robin dispatch deals every XCD the same mix.
 //
-// Inside a wave, as in the bf16 kernel: transposed scores S^T = K Q^T so each
-// lane owns one query column, and O^T = V^T P^T. With K = 2 per instruction
-// each 32-lane half contributes one contraction index per step, so:
-//  * the score product walks r in R/2 steps, lane half h covering dims
-//    [h R/2, (h+1) R/2) (contiguous in the K row, read 16 bytes at a time);
-//  * the value product walks the 32 keys of a block in 16 steps, lane half h
-//    supplying the key that its accumulator register already holds, so P^T is
-//    used in place with no repacking. V is stored transposed ([d_v][keys] fp32,
-//    natural key order) so four consecutive steps' operands are one 16-byte read.
-// A wave loads its next tile into registers while it computes the current one.
+// Inside a wave: transposed scores S^T = K Q^T per 16-key block, so lane (g, n)
+// of lane group g = lane / 16 serves query n = lane % 16, and O^T = V^T P^T.
+// Each instruction contracts 4 indices, one per lane group, so:
+//  * the score product walks r in R/4 steps, lane group g covering dims
+//    [g R/4, (g+1) R/4) (contiguous in the K row, read 16 bytes at a time);
+//  * the value product takes, in step i of a key block, keys 4 g + i: the keys
+//    whose scores lane group g already holds in accumulator register i, so P^T
+//    is used in place with no repacking. V is stored transposed ([d_v][keys]
+//    fp32, natural key order) so one 16-byte read gives a lane the operands of
+//    four steps.
+// Row maxima and sums reduce over the four lane groups of a query (lane
+// n, n + 16, n + 32, n + 48). A wave loads its next tile into registers while
+// it computes the current one.
 #include "tk_device.hpp"
 #include "tk_internal.hpp"
 
@@ -32,9 +36,9 @@ namespace {
 
 constexpr int kWaves = 4;
 constexpr int kThreads = 64 * kWaves;
-constexpr int kRows = 32;  // query rows per workgroup
+constexpr int kRows = 16;  // query rows per workgroup
 
-// Keys per tile: one 32-key block. A wave's tile then costs 32 (R + DV) / 64
+// Keys per tile: 32 (two 16-key blocks). A wave's tile then costs 32 (R + DV) / 64
 // floats of prefetch registers per lane, and at the GPT-2 shape (r 16, d_v 64)
 // the workgroup's four tiles take 45 KB of LDS, so three workgroups share a CU
 // and one wave's softmax overlaps another's matrix products (with 64-key tiles
@@ -147,14 +151,15 @@ union alignas(16) Smem {
 template <int R, int DV>
 __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillParams p) {
     using T = WaveTile<R, DV>;
-    constexpr int HR = R / 2;  // score-product steps (dims per lane half)
-    constexpr int DBLK = DV / 32;
-    constexpr int BN = T::BN, KB = T::KB, KS = T::KS, VS = T::VS;
+    constexpr int RS = R / 4;     // score-product steps: lane group g covers dims [g RS, (g + 1) RS)
+    constexpr int DBLK = DV / 16;  // 16-row blocks of O^T
+    constexpr int BN = T::BN, KS = T::KS, VS = T::VS;
+    static_assert(BN == 32, "a tile is two 16-key blocks");
     __shared__ Smem<R, DV> sm;
 
     const int tid = threadIdx.x;
     const int lane = tid & 63, wave = tid >> 6;
-    const int half = lane >> 5, col = lane & 31;
+    const int grp = lane >> 4, n = lane & 15;  // lane group, and the query (B column) the lane serves
 
     // workgroup -> (query block, head, sequence): ranked by causal prefix length,
     // longest first, with the heads and sequences of one rank adjacent, so that the
@@ -175,10 +180,16 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillP
     const float* vg = (const float*)p.v + ((size_t)b * p.Hkv + g) * p.Sk * DV;
     float* og = (float*)p.o + ((size_t)b * p.Hq + h) * p.Sq * DV;
 
-    const int qrow = q0 + col;
-    float qreg[HR];
+    const int qrow = q0 + n;
+    float qreg[RS];
 #pragma unroll
-    for (int s = 0; s < HR; ++s) qreg[s] = qrow < p.Sq ? qg[(size_t)qrow * R + half * HR + s] : 0.f;
+    for (int s4 = 0; s4 < RS; s4 += 4) {
+        const float4 w = qrow < p.Sq ? *(const float4*)(qg + (size_t)qrow * R + grp * RS + s4) : make_float4(0, 0, 0, 0);
+        qreg[s4] = w.x;
+        qreg[s4 + 1] = w.y;
+        qreg[s4 + 2] = w.z;
+        qreg[s4 + 3] = w.w;
+    }
 
     int key_end = p.Sk;
     if (p.causal) {
@@ -187,13 +198,11 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillP
     }
     const int ntiles = (key_end + BN - 1) / BN;
 
-    f32x16 o[DBLK];
+    f32x4 o[DBLK];
 #pragma unroll
-    for (int d = 0; d < DBLK; ++d)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) o[d][v] = 0.f;
-    float m_ref = -INFINITY;  // this row's reference maximum (log2 domain)
-    float lsum = 0.f;         // this lane half's share of the row sum
+    for (int d = 0; d < DBLK; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+    float m_ref = -INFINITY;  // this query's reference maximum (log2 domain), the same in its 4 lanes
+    float lsum = 0.f;         // this lane's share of the query's row sum
     const float c = p.qscale;
 
     T& tile = sm.tile[wave];
@@ -206,19 +215,19 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillP
         wave_lds_sync();
         if (t + kWaves < ntiles) load_tile<R, DV>(regs, kg, vg, base + kWaves * BN, p.Sk, lane);
 
-        f32x16 s[KB];
+        // S^T = K Q^T per 16-key block: lane (g, n) ends with keys 16 kb + 4 g + i of query n
+        f32x4 s[2];
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
+        for (int kb = 0; kb < 2; ++kb) {
+            s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const float* krow = tile.k + (kb * 16 + n) * KS + grp * RS;
 #pragma unroll
-            for (int v = 0; v < 16; ++v) s[kb][v] = 0.f;
-            const float* krow = tile.k + (kb * 32 + col) * KS + half * HR;
-#pragma unroll
-            for (int s4 = 0; s4 < HR; s4 += 4) {
+            for (int s4 = 0; s4 < RS; s4 += 4) {
                 const float4 a = *(const float4*)(krow + s4);
-                s[kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.x, qreg[s4 + 0], s[kb], 0, 0, 0);
-                s[kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.y, qreg[s4 + 1], s[kb], 0, 0, 0);
-                s[kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.z, qreg[s4 + 2], s[kb], 0, 0, 0);
-                s[kb] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.w, qreg[s4 + 3], s[kb], 0, 0, 0);
+                s[kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, qreg[s4 + 0], s[kb], 0, 0, 0);
+                s[kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, qreg[s4 + 1], s[kb], 0, 0, 0);
+                s[kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, qreg[s4 + 2], s[kb], 0, 0, 0);
+                s[kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, qreg[s4 + 3], s[kb], 0, 0, 0);
             }
         }
         // causal / ragged-tail mask, only where the tile crosses it
@@ -227,72 +236,64 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillP
             const int limit = p.causal ? qrow + off : p.Sk - 1;
             const int lim = limit < p.Sk - 1 ? limit : p.Sk - 1;
 #pragma unroll
-            for (int kb = 0; kb < KB; ++kb)
+            for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int key = base + kb * 32 + 8 * (v >> 2) + 4 * half + (v & 3);
-                    if (key > lim) s[kb][v] = -INFINITY;
+                for (int i = 0; i < 4; ++i) {
+                    const int key = base + kb * 16 + 4 * grp + i;
+                    if (key > lim) s[kb][i] = -INFINITY;
                 }
         }
-        float mx = s[0][0];
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[kb][v]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
+                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+        mx = strided_max<16>(mx);  // over the query's 4 lane groups
         const float mx2 = mx * c;
-        // each row moves its own reference only, when its maximum exceeds it by
+        // each query moves its own reference only, when its maximum exceeds it by
         // more than 8 (a factor of 256); the branch is taken by the whole wave
-        // when any row needs it
+        // when any query needs it
         const bool need = mx2 > m_ref + 8.f;
         if (__any(need)) {
             const float alpha = need ? exp2_fast(m_ref - mx2) : 1.f;
             m_ref = need ? mx2 : m_ref;
             lsum *= alpha;
 #pragma unroll
-            for (int d = 0; d < DBLK; ++d)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) o[d][v] *= alpha;
+            for (int d = 0; d < DBLK; ++d) o[d] *= alpha;
         }
-        // a row with no reference yet has seen no visible key: its scores are all
+        // a query with no reference yet has seen no visible key: its scores are all
         // -inf here (a wave's first tile can lie past a row's causal limit), and
         // exponentiating against 0 gives them weight 0 instead of NaN
         const float m_use = m_ref == -INFINITY ? 0.f : m_ref;
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                s[kb][v] = exp2_fast(fmaf(s[kb][v], c, -m_use));
-                lsum += s[kb][v];
+            for (int i = 0; i < 4; ++i) {
+                s[kb][i] = exp2_fast(fmaf(s[kb][i], c, -m_use));
+                lsum += s[kb][i];
             }
-        // O^T += V^T P^T, one key per lane half per step
+        // O^T += V^T P^T: contraction step i of block kb takes keys 16 kb + 4 g + i,
+        // which lane group g already holds in register i of its score block
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
+        for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int d = 0; d < DBLK; ++d) {
-                const float* vrow = tile.vt + (d * 32 + col) * VS + kb * 32 + 4 * half;
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const float4 a = *(const float4*)(vrow + 8 * j);
-                    o[d] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.x, s[kb][4 * j + 0], o[d], 0, 0, 0);
-                    o[d] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.y, s[kb][4 * j + 1], o[d], 0, 0, 0);
-                    o[d] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.z, s[kb][4 * j + 2], o[d], 0, 0, 0);
-                    o[d] = __builtin_amdgcn_mfma_f32_32x32x2f32(a.w, s[kb][4 * j + 3], o[d], 0, 0, 0);
-                }
+                const float4 a = *(const float4*)(tile.vt + (d * 16 + n) * VS + kb * 16 + 4 * grp);
+                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, s[kb][0], o[d], 0, 0, 0);
+                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, s[kb][1], o[d], 0, 0, 0);
+                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, s[kb][2], o[d], 0, 0, 0);
+                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, s[kb][3], o[d], 0, 0, 0);
             }
         wave_lds_sync();  // the tile's operand reads are done before the next store
     }
 
     // ---- merge the 4 waves' partial results (log-sum-exp rule) and write the rows
-    const float ltot = lsum + __shfl_xor(lsum, 32);
+    const float ltot = strided_sum<16>(lsum);
     __syncthreads();  // every wave is done with its tile: the LDS becomes the merge area
 #pragma unroll
     for (int d = 0; d < DBLK; ++d)
 #pragma unroll
-        for (int v = 0; v < 16; ++v) sm.merge.o[wave][d * 32 + 8 * (v >> 2) + 4 * half + (v & 3)][col] = o[d][v];
-    if (half == 0) {
-        sm.merge.m[wave][col] = m_ref;
-        sm.merge.l[wave][col] = ltot;
+        for (int i = 0; i < 4; ++i) sm.merge.o[wave][d * 16 + 4 * grp + i][n] = o[d][i];
+    if (grp == 0) {
+        sm.merge.m[wave][n] = m_ref;
+        sm.merge.l[wave][n] = ltot;
     }
     __syncthreads();
     for (int e = tid; e < kRows * DV; e += kThreads) {
