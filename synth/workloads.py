@@ -154,8 +154,13 @@ def quantize_int4(k: torch.Tensor):
     return (n[..., 0::2] | (n[..., 1::2] << 4)).to(torch.uint8), scale
 
 
-def make_prefill(spec: PrefillSpec, device="cpu", structured: bool = False):
-    """Q, K, V of a prefill workload, in the workload's dtype, on ``device``."""
+def make_prefill(spec: PrefillSpec, device="cpu", structured: bool = False, needle_logit: Optional[float] = None):
+    """Q, K, V of a prefill workload, in the workload's dtype, on ``device``.
+
+    ``structured`` plants the copy-back pattern; by default its planted logit is
+    about 2 sqrt(r) over noise logits of standard deviation 2 (rows close to
+    one-hot). ``needle_logit`` sets the planted logit's expected size instead
+    (noise standard deviation needle_logit / sqrt(r)), for moderately peaked rows."""
     B, Hq, Hkv, Sq, Sk, r, dv = spec.batch, spec.h_q, spec.h_kv, spec.seq_q, spec.seq_k, spec.r, spec.d_v
     dt = torch.float32 if spec.dtype == "f32" else torch.bfloat16
     q = _draw(spec.config_id, T_Q, (B, Hq, Sq, r), device, spec.amp)
@@ -168,6 +173,8 @@ def make_prefill(spec: PrefillSpec, device="cpu", structured: bool = False):
         G = Hq // Hkv
         off = 8 + (Sk - Sq)
         lam = 2.0 / (spec.amp * spec.amp * math.sqrt(r) * spec.softmax_scale)
+        if needle_logit is not None:
+            lam = needle_logit / (spec.amp * spec.amp * r * spec.softmax_scale)
         kk = k.to(torch.float32).repeat_interleave(G, dim=1)  # [B, Hq, Sk, r]
         i0 = max(0, -off + 0)
         rows = torch.arange(Sq, device=device)

@@ -78,12 +78,16 @@ def prefill_oracle(p, spec):
 
 
 def prefill_rows_oracle(p, spec, b: int, rows):
-    """Oracle for selected causal query rows of sequence b, all heads: row i of a
-    causal prefill is a decode over keys 0..i + (Sk - Sq)."""
+    """Oracle for selected query rows of sequence b, all heads: row i of a causal
+    prefill is a decode over keys 0..i + (Sk - Sq). The sequence's own K and V
+    serve every row as one cache page of Sk tokens (block table all zeros), so
+    nothing is copied per row."""
     q = p["q"][b, :, rows].permute(1, 0, 2).contiguous().cpu()   # [n, Hq, r]
     n = len(rows)
-    k = p["k"][b:b + 1].cpu().expand(n, -1, -1, -1).contiguous()
-    v = p["v"][b:b + 1].cpu().expand(n, -1, -1, -1).contiguous()
+    k = p["k"][b:b + 1].cpu().contiguous()                       # one page [1, Hkv, Sk, r]
+    v = p["v"][b:b + 1].cpu().contiguous()
     off = spec.seq_k - spec.seq_q
     lens = torch.tensor([i + off + 1 if spec.causal else spec.seq_k for i in rows], dtype=torch.int32)
-    return orc.decode(q, k, v, lens, scale=spec.softmax_scale)   # [n, Hq, dv]
+    table = torch.zeros(n, 1, dtype=torch.int32)
+    return orc.decode(q, k, v, lens, scale=spec.softmax_scale, block_table=table,
+                      block_size=spec.seq_k)                      # [n, Hq, dv]

@@ -1,7 +1,8 @@
 """Decode parity on the GPU: tk_attn_decode against the fp64 oracle on the same
 seeded inputs, at small sweep sizes (every output), at the full workload sizes
-in the launch configuration the benchmark times (every output of the
-batch-16 Mistral step; sampled sequences of the long-context and fp8 steps),
+in the launch configuration the benchmark times (every output of every
+sequence, i.i.d. and structured, for the batch-16, long-context paged, fp8-key
+and 4-bit-key steps),
 plus invariants that must hold at any size."""
 import pytest
 import torch
@@ -74,23 +75,26 @@ def test_mistral_decode_b16_full(name):
         say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
 
 
+@pytest.mark.parametrize("structured", [False, True])
 @pytest.mark.parametrize("name", ["longctx_paged_decode", "longctx_paged_decode_fullkey"])
-def test_longctx_paged_decode_full_sampled(name):
+def test_longctx_paged_decode_full(name, structured):
     """Context 131072 in 256-token pages with a permuted table, thin keys (r 32) and the
-    full-key control (r 128); oracle on 2 of 8 sequences."""
+    full-key control (r 128): every output of all 8 sequences."""
     spec = {**WORKLOADS, **FULLKEY}[name]
-    out, ref = run_case(spec, structured=True, batches=[0, 7], on_gpu_inputs=True)
-    mx, rel = gate(out, ref, "bf16", name)
+    out, ref = run_case(spec, structured=structured, on_gpu_inputs=True)
+    mx, rel = gate(out, ref, "bf16", f"{name} structured={structured}")
     say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
 
 
+@pytest.mark.parametrize("structured", [False, True])
 @pytest.mark.parametrize("name", ["fp8key_decode", "int4key_decode", "int4key_decode_fullkey"])
-def test_quantised_key_decode_full_sampled(name):
+def test_quantised_key_decode_full(name, structured):
     """Batch 32, context 32768, E4M3 or 4-bit keys with per-token-head scales, and the
-    standard-key control of that shape (r 128, bf16); oracle on 3 sequences."""
+    standard-key control of that shape (r 128, bf16): every output of all 32
+    sequences."""
     spec = {**WORKLOADS, **INT4KEY, **FULLKEY}[name]
-    out, ref = run_case(spec, structured=True, batches=[0, 13, 31], on_gpu_inputs=True)
-    mx, rel = gate(out, ref, spec.k_dtype, name)
+    out, ref = run_case(spec, structured=structured, on_gpu_inputs=True)
+    mx, rel = gate(out, ref, spec.k_dtype, f"{name} structured={structured}")
     say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
 
 

@@ -1,6 +1,6 @@
 """Prefill parity on the GPU: tk_attn_prefill against the fp64 oracle on the same
 seeded inputs — every output at sweep sizes and at the GPT-2 fp32 size, and
-sampled rows (all heads) at the Mistral 8192-token size in the launch
+65 rows of every sequence (all heads) at the Mistral 8192-token size in the launch
 configuration the benchmark times — plus causal invariants."""
 import pytest
 import torch
@@ -64,22 +64,29 @@ def test_gpt2_prefill_f32_full():
         say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
 
 
-ROWS = [0, 1, 7, 8, 31, 32, 63, 64, 65, 127, 128, 1000, 4095, 4096, 8190, 8191]
+# first and last row of 32-row wave blocks (and of 64-key tiles) at causal depths
+# from the first tile to the last, plus interior rows: 65 rows per sequence
+BLOCKS = [0, 1, 2, 3, 7, 15, 31, 32, 63, 64, 100, 127, 128, 129, 191, 200, 223, 240, 250, 253, 254, 255]
+ROWS = sorted({32 * kb + d for kb in BLOCKS for d in (0, 31)} | {5, 17, 47, 48, 95, 1000, 2049, 3071, 4096,
+                                                                    4111, 5000, 6143, 7000, 7777, 8000,
+                                                                    8100, 8129, 8150, 8160, 8175, 8180,
+                                                                    8185, 8189, 8190, 2, 33, 1023, 1024, 4095})
 
 
 @pytest.mark.parametrize("structured", [False, True])
 @pytest.mark.parametrize("name", ["mistral_prefill_s8192", "mistral_prefill_s8192_fullkey"])
 def test_mistral_prefill_s8192_full_sampled(name, structured):
     """Batch 4, 32/8 heads, 8192 tokens, d_v 128, bf16, thin keys (r 32) and the
-    full-key control (r 128): the whole call on the GPU, 16 rows of 2 sequences (all
-    heads) against the oracle."""
+    full-key control (r 128): the whole call on the GPU, 65 rows of every sequence
+    (all heads) against the oracle."""
     dev = device()
     spec = {**WORKLOADS, **FULLKEY}[name]
     p = make_prefill(spec, device=dev, structured=structured)
     say(f"prefill full {spec.name} structured={structured}")
     out = prefill_on_gpu(p, spec, dev)
     torch.cuda.synchronize()
-    for b in (0, 3):
+    assert len(ROWS) >= 64
+    for b in range(spec.batch):
         ref = prefill_rows_oracle(p, spec, b, ROWS)                  # [n, Hq, dv]
         got = out[b, :, ROWS].permute(1, 0, 2)
         mx, rel = gate(got, ref, "bf16", f"b={b}")
