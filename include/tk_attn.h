@@ -184,6 +184,32 @@ tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache
                          void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 /*
+ * tk_attn_decode without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation). Arguments, layouts, results and errors are
+ * those of tk_attn_decode, and the same kernels run with the same split, so
+ * outputs are bitwise equal to tk_attn_decode's.
+ *
+ * Instead of a caller's workspace the call uses a fixed device array inside the
+ * library: 4 MiB per GPU, held from the first call on that GPU until the process
+ * ends. Every supported shape fits (a split context has fewer than 4096
+ * (sequence, head, split) partial rows); a call that would need more returns
+ * TK_ERR_WORKSPACE before touching the GPU. On the first call on a device (the
+ * current device, which must be the stream's device, else TK_ERR_INVALID_ARG)
+ * the library looks up that device's copy and clears its counters with a small
+ * kernel on `stream`; every completed call leaves them zero again.
+ * The call allocates nothing and makes no hipMalloc or hipFree. All calls on one
+ * GPU share the array: calls that may overlap on one GPU (different streams,
+ * host threads or processes) race and must be serialised by the caller.
+ */
+tk_status tk_attn_decode_noalloc(const void* Q, const void* K_cache, const void* V_cache, void* O,
+                                 int batch, int H_q, int H_kv, const int32_t* ctx_lens, int max_ctx,
+                                 int r, int d_v, float scale,
+                                 tk_dtype k_dtype, const float* k_scale,
+                                 const int32_t* block_table, int block_size, int max_blocks_per_seq,
+                                 int num_blocks, hipStream_t stream);
+
+/*
  * Append n_new tokens per sequence to a thin-key / full-value cache: the write
  * that precedes decode (the thin-K / full-V cache of Sec. 2.4, Eq. 9). Token t
  * of sequence b and KV head g is stored at cache position positions[b] + t.

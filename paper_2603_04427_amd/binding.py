@@ -30,6 +30,8 @@ SIGNATURES = {
     "tk_attn_decode_workspace_bytes": ([_i, _i, _i, _i, _i], _sz),
     "tk_attn_decode": ([_vp, _vp, _vp, _vp, _i, _i, _i, _vp, _i, _i, _i, _f, _i, _vp, _vp, _i, _i, _i,
                         _vp, _sz, _vp], _i),
+    "tk_attn_decode_noalloc": ([_vp, _vp, _vp, _vp, _i, _i, _i, _vp, _i, _i, _i, _f, _i, _vp, _vp, _i, _i, _i,
+                                _vp], _i),
     "tk_cache_append": ([_vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _i, _vp, _vp, _i, _i, _i, _vp], _i),
     "tk_status_str": ([_i], ctypes.c_char_p),
     "tk_version": ([], _i),
@@ -231,10 +233,11 @@ def prepare_decode(Q: torch.Tensor, K_cache: torch.Tensor, V_cache: torch.Tensor
                    max_ctx: Optional[int] = None, scale: float = 0.0, k_scale: Optional[torch.Tensor] = None,
                    block_table: Optional[torch.Tensor] = None, block_size: int = 0,
                    workspace: Optional[torch.Tensor] = None, O: Optional[torch.Tensor] = None,
-                   stream=None) -> PreparedCall:
+                   stream=None, noalloc: bool = False) -> PreparedCall:
     """One decode step, marshalled. Q [B,Hq,r] bf16; K_cache bf16, uint8 E4M3 codes or uint8 packed 4-bit
     codes [.., r/2] (quantised keys with k_scale fp32); contiguous [B,Hkv,max_ctx,*] or paged
-    [nblk,Hkv,bs,*] with block_table [B, mb] int32."""
+    [nblk,Hkv,bs,*] with block_table [B, mb] int32. With ``noalloc`` the call goes to
+    tk_attn_decode_noalloc (the library's fixed scratch; no workspace)."""
     _check(Q, "Q", (torch.bfloat16,), 3)
     _check(K_cache, "K_cache", (torch.bfloat16, torch.uint8, torch.float8_e4m3fn), 4)
     _check(V_cache, "V_cache", (torch.bfloat16,), 4)
@@ -274,17 +277,22 @@ def prepare_decode(Q: torch.Tensor, K_cache: torch.Tensor, V_cache: torch.Tensor
         max_ctx = cap
     if max_ctx > cap:
         raise ValueError("max_ctx exceeds the cache capacity")
+    if O is None:
+        O = torch.empty(B, Hq, dv, dtype=torch.bfloat16, device=Q.device)
+    _check(O, "O", (torch.bfloat16,), 3)
+    head = (_ptr(Q), _ptr(K_cache), _ptr(V_cache), _ptr(O), B, Hq, Hkv, _ptr(ctx_lens), int(max_ctx), r, dv,
+            float(scale), kf, _ptr(k_scale), _ptr(block_table), int(block_size), int(mb), int(nblk))
+    if noalloc:
+        if workspace is not None:
+            raise ValueError("tk_attn_decode_noalloc takes no workspace")
+        return PreparedCall("tk_attn_decode_noalloc", head + (_stream(stream),),
+                            (Q, K_cache, V_cache, ctx_lens, k_scale, block_table, O))
     need = tk_attn_decode_workspace_bytes(B, Hq, Hkv, max_ctx, dv)
     if workspace is None:
         workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=Q.device)
     if workspace.device.type != "cuda":
         raise ValueError("workspace must be on the GPU")
-    if O is None:
-        O = torch.empty(B, Hq, dv, dtype=torch.bfloat16, device=Q.device)
-    _check(O, "O", (torch.bfloat16,), 3)
-    args = (_ptr(Q), _ptr(K_cache), _ptr(V_cache), _ptr(O), B, Hq, Hkv, _ptr(ctx_lens), int(max_ctx), r, dv,
-            float(scale), kf, _ptr(k_scale), _ptr(block_table), int(block_size),
-            int(mb), int(nblk), _ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
+    args = head + (_ptr(workspace), workspace.numel() * workspace.element_size(), _stream(stream))
     return PreparedCall("tk_attn_decode", args, (Q, K_cache, V_cache, ctx_lens, k_scale, block_table, workspace, O))
 
 
@@ -299,6 +307,16 @@ def tk_attn_decode(Q: torch.Tensor, K_cache: torch.Tensor, V_cache: torch.Tensor
     A workspace passed in must have been zeroed before its first use (see include/tk_attn.h)."""
     return prepare_decode(Q, K_cache, V_cache, ctx_lens, max_ctx, scale, k_scale, block_table, block_size,
                           workspace, O, stream)()
+
+
+def tk_attn_decode_noalloc(Q: torch.Tensor, K_cache: torch.Tensor, V_cache: torch.Tensor, ctx_lens: torch.Tensor,
+                           max_ctx: Optional[int] = None, scale: float = 0.0, k_scale: Optional[torch.Tensor] = None,
+                           block_table: Optional[torch.Tensor] = None, block_size: int = 0,
+                           O: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """tk_attn_decode on the library's fixed scratch: the C call allocates nothing (pass O to keep this
+    wrapper from allocating the output). Calls that may overlap on one GPU race (see include/tk_attn.h)."""
+    return prepare_decode(Q, K_cache, V_cache, ctx_lens, max_ctx, scale, k_scale, block_table, block_size,
+                          None, O, stream, noalloc=True)()
 
 
 def prepare_cache_append(K_new: torch.Tensor, V_new: torch.Tensor, positions: torch.Tensor,

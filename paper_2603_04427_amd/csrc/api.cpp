@@ -62,6 +62,77 @@ tk_status prefill_impl(const void* Q, const void* K, const void* V, void* O, flo
     return dtype == TK_BF16 ? tk::launch_prefill_bf16(p, r, d_v, stream) : tk::launch_prefill_f32(p, r, d_v, stream);
 }
 
+// Decode with a caller's workspace, or (use_scratch) with the library's fixed
+// scratch, which then needs only the bytes the plan touches: the counters, and
+// the partials when the context is split.
+tk_status decode_impl(const void* Q, const void* K_cache, const void* V_cache, void* O, int batch, int H_q,
+                      int H_kv, const int32_t* ctx_lens, int max_ctx, int r, int d_v, float scale, tk_dtype k_dtype,
+                      const float* k_scale, const int32_t* block_table, int block_size, int max_blocks_per_seq,
+                      int num_blocks, void* workspace, size_t workspace_bytes, bool use_scratch,
+                      hipStream_t stream) {
+    if (batch < 0 || H_q <= 0 || H_kv <= 0 || max_ctx < 0 || r <= 0 || d_v <= 0) return TK_ERR_INVALID_ARG;
+    if (H_q % H_kv != 0) return TK_ERR_INVALID_ARG;
+    if (k_dtype != TK_BF16 && k_dtype != TK_FP8_E4M3 && k_dtype != TK_INT4)
+        return k_dtype == TK_F32 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
+    const bool quantised = k_dtype != TK_BF16;
+    if (quantised != (k_scale != nullptr)) return TK_ERR_INVALID_ARG;  // scales iff quantised keys
+    const bool paged = block_table != nullptr;
+    int bs_log2 = 0;
+    if (paged) {
+        if (block_size <= 0 || max_blocks_per_seq <= 0 || num_blocks <= 0) return TK_ERR_INVALID_ARG;
+        if ((long)block_size * max_blocks_per_seq < max_ctx) return TK_ERR_INVALID_ARG;
+        bs_log2 = log2_exact(block_size);
+        if (bs_log2 < 0 || block_size < 64) return TK_ERR_UNSUPPORTED;
+    } else if (block_size != 0 || max_blocks_per_seq != 0 || num_blocks != 0) {
+        return TK_ERR_INVALID_ARG;  // layout arguments without a table
+    }
+    if (batch == 0) return TK_OK;
+    if (!Q || !K_cache || !V_cache || !O || !ctx_lens) return TK_ERR_INVALID_ARG;
+    if (!aligned16(Q) || !aligned16(K_cache) || !aligned16(V_cache) || !aligned16(O)) return TK_ERR_INVALID_ARG;
+    if (!supported_r(r) || !supported_dv(d_v)) return TK_ERR_UNSUPPORTED;
+    if (batch > kMaxGrid) return TK_ERR_UNSUPPORTED;
+
+    const tk::DecodePlan pl = tk::plan_decode(batch, H_q, H_kv, max_ctx, d_v);
+    if ((long)H_kv * (H_q / H_kv / pl.heads_per_group) > kMaxGrid || pl.n_split > 0x7fffffff)
+        return TK_ERR_UNSUPPORTED;
+    // wide keys leave no registers for 8 heads per workgroup: use groups of 4
+    const int hg = (r >= 64 && pl.heads_per_group > 4) ? 4 : pl.heads_per_group;
+    // a split context needs one arrival counter per (sequence, head group)
+    if (pl.n_split > 1 && (size_t)batch * H_kv * (H_q / H_kv / hg) * sizeof(unsigned) > pl.counter_bytes)
+        return TK_ERR_UNSUPPORTED;
+    if (use_scratch) {
+        const size_t need = pl.n_split > 1 ? pl.ws_bytes : pl.counter_bytes;
+        if (need > tk::kDecodeScratchBytes) return TK_ERR_WORKSPACE;
+        const tk_status st = tk::decode_scratch(stream, &workspace);  // first HIP call of this path
+        if (st != TK_OK) return st;
+    } else if (!workspace || workspace_bytes < pl.ws_bytes || ((uintptr_t)workspace & 255u)) {
+        return TK_ERR_WORKSPACE;
+    }
+
+    tk::DecodeParams p{};
+    p.q = (const uint16_t*)Q;
+    p.k = (const uint8_t*)K_cache;
+    p.k_scale = k_scale;
+    p.v = (const uint16_t*)V_cache;
+    p.ctx_lens = ctx_lens;
+    p.block_table = block_table;
+    p.counters = (unsigned*)workspace;
+    p.ws = (float*)((char*)workspace + pl.counter_bytes);
+    p.o = (uint16_t*)O;
+    p.B = batch;
+    p.Hq = H_q;
+    p.Hkv = H_kv;
+    p.G = H_q / H_kv;
+    p.max_ctx = max_ctx;
+    p.bs_log2 = bs_log2;
+    p.mb = paged ? max_blocks_per_seq : 0;
+    p.num_blocks = paged ? num_blocks : 0;
+    p.n_split = pl.n_split;
+    p.split_len = pl.split_len;
+    p.qscale = resolve_scale(scale, r) * tk::kLog2e;
+    return tk::launch_decode(p, r, d_v, hg, key_format(k_dtype), paged, stream);
+}
+
 }  // namespace
 
 extern "C" {
@@ -156,60 +227,17 @@ tk_status tk_attn_decode(const void* Q, const void* K_cache, const void* V_cache
                          tk_dtype k_dtype, const float* k_scale, const int32_t* block_table, int block_size,
                          int max_blocks_per_seq, int num_blocks, void* workspace, size_t workspace_bytes,
                          hipStream_t stream) {
-    if (batch < 0 || H_q <= 0 || H_kv <= 0 || max_ctx < 0 || r <= 0 || d_v <= 0) return TK_ERR_INVALID_ARG;
-    if (H_q % H_kv != 0) return TK_ERR_INVALID_ARG;
-    if (k_dtype != TK_BF16 && k_dtype != TK_FP8_E4M3 && k_dtype != TK_INT4)
-        return k_dtype == TK_F32 ? TK_ERR_UNSUPPORTED : TK_ERR_INVALID_ARG;
-    const bool quantised = k_dtype != TK_BF16;
-    if (quantised != (k_scale != nullptr)) return TK_ERR_INVALID_ARG;  // scales iff quantised keys
-    const bool paged = block_table != nullptr;
-    int bs_log2 = 0;
-    if (paged) {
-        if (block_size <= 0 || max_blocks_per_seq <= 0 || num_blocks <= 0) return TK_ERR_INVALID_ARG;
-        if ((long)block_size * max_blocks_per_seq < max_ctx) return TK_ERR_INVALID_ARG;
-        bs_log2 = log2_exact(block_size);
-        if (bs_log2 < 0 || block_size < 64) return TK_ERR_UNSUPPORTED;
-    } else if (block_size != 0 || max_blocks_per_seq != 0 || num_blocks != 0) {
-        return TK_ERR_INVALID_ARG;  // layout arguments without a table
-    }
-    if (batch == 0) return TK_OK;
-    if (!Q || !K_cache || !V_cache || !O || !ctx_lens) return TK_ERR_INVALID_ARG;
-    if (!aligned16(Q) || !aligned16(K_cache) || !aligned16(V_cache) || !aligned16(O)) return TK_ERR_INVALID_ARG;
-    if (!supported_r(r) || !supported_dv(d_v)) return TK_ERR_UNSUPPORTED;
-    if (batch > kMaxGrid) return TK_ERR_UNSUPPORTED;
+    return decode_impl(Q, K_cache, V_cache, O, batch, H_q, H_kv, ctx_lens, max_ctx, r, d_v, scale, k_dtype, k_scale,
+                       block_table, block_size, max_blocks_per_seq, num_blocks, workspace, workspace_bytes, false,
+                       stream);
+}
 
-    const tk::DecodePlan pl = tk::plan_decode(batch, H_q, H_kv, max_ctx, d_v);
-    if ((long)H_kv * (H_q / H_kv / pl.heads_per_group) > kMaxGrid || pl.n_split > 0x7fffffff)
-        return TK_ERR_UNSUPPORTED;
-    if (!workspace || workspace_bytes < pl.ws_bytes || ((uintptr_t)workspace & 255u)) return TK_ERR_WORKSPACE;
-
-    tk::DecodeParams p{};
-    p.q = (const uint16_t*)Q;
-    p.k = (const uint8_t*)K_cache;
-    p.k_scale = k_scale;
-    p.v = (const uint16_t*)V_cache;
-    p.ctx_lens = ctx_lens;
-    p.block_table = block_table;
-    p.counters = (unsigned*)workspace;
-    p.ws = (float*)((char*)workspace + pl.counter_bytes);
-    p.o = (uint16_t*)O;
-    p.B = batch;
-    p.Hq = H_q;
-    p.Hkv = H_kv;
-    p.G = H_q / H_kv;
-    p.max_ctx = max_ctx;
-    p.bs_log2 = bs_log2;
-    p.mb = paged ? max_blocks_per_seq : 0;
-    p.num_blocks = paged ? num_blocks : 0;
-    p.n_split = pl.n_split;
-    p.split_len = pl.split_len;
-    p.qscale = resolve_scale(scale, r) * tk::kLog2e;
-    // wide keys leave no registers for 8 heads per workgroup: use groups of 4
-    const int hg = (r >= 64 && pl.heads_per_group > 4) ? 4 : pl.heads_per_group;
-    // a split context needs one arrival counter per (sequence, head group)
-    if (pl.n_split > 1 && (size_t)batch * H_kv * (H_q / H_kv / hg) * sizeof(unsigned) > pl.counter_bytes)
-        return TK_ERR_UNSUPPORTED;
-    return tk::launch_decode(p, r, d_v, hg, key_format(k_dtype), paged, stream);
+tk_status tk_attn_decode_noalloc(const void* Q, const void* K_cache, const void* V_cache, void* O, int batch,
+                                 int H_q, int H_kv, const int32_t* ctx_lens, int max_ctx, int r, int d_v,
+                                 float scale, tk_dtype k_dtype, const float* k_scale, const int32_t* block_table,
+                                 int block_size, int max_blocks_per_seq, int num_blocks, hipStream_t stream) {
+    return decode_impl(Q, K_cache, V_cache, O, batch, H_q, H_kv, ctx_lens, max_ctx, r, d_v, scale, k_dtype, k_scale,
+                       block_table, block_size, max_blocks_per_seq, num_blocks, nullptr, 0, true, stream);
 }
 
 tk_status tk_cache_append(const void* K_new, const void* V_new, int batch, int H_kv, int n_new, int r, int d_v,

@@ -26,6 +26,7 @@
 
 #include <math.h>
 
+#include <mutex>
 #include <type_traits>
 
 #ifndef TK_DECODE_TARGET_GROUPS
@@ -654,6 +655,46 @@ DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV) {
     pl.counter_bytes = kCounterRegionBytes;
     pl.ws_bytes = pl.counter_bytes + (size_t)B * Hq * pl.n_split * (DV + 2) * sizeof(float);
     return pl;
+}
+
+// ------------------------------------------------------------------ fixed scratch
+
+// Callers that cannot allocate (graph capture, tight serving loops) use this
+// array instead of a workspace of their own. Host code never passes its name:
+// it looks up the device address once per device and uses that.
+static __device__ __align__(256) unsigned char scratch[kDecodeScratchBytes];
+static_assert(kCounterRegionBytes <= kDecodeScratchBytes, "the counters fit the scratch");
+
+__global__ void zero_words_kernel(unsigned* p, int n) {
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) p[i] = 0u;
+}
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch[kMaxDevices];  // device address of each device's copy, once looked up
+}  // namespace
+
+tk_status decode_scratch(hipStream_t stream, void** ptr) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TK_ERR_HIP;
+    int sdev = -1;
+    if (hipStreamGetDevice(stream, &sdev) != hipSuccess) return TK_ERR_HIP;
+    if (sdev != dev) return TK_ERR_INVALID_ARG;  // the scratch used is the current device's
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch[dev]) {
+        void* addr = nullptr;
+        if (hipGetSymbolAddress(&addr, HIP_SYMBOL(scratch)) != hipSuccess || !addr) return TK_ERR_HIP;
+        // the arrival counters must start at zero; completed calls leave them zero
+        const int words = (int)(kCounterRegionBytes / sizeof(unsigned));
+        hipLaunchKernelGGL(zero_words_kernel, dim3((words + 255) / 256), dim3(256), 0, stream, (unsigned*)addr,
+                           words);
+        if (hipGetLastError() != hipSuccess) return TK_ERR_HIP;
+        g_scratch[dev] = addr;
+    }
+    *ptr = g_scratch[dev];
+    return TK_OK;
 }
 
 // ------------------------------------------------------------------ dispatch

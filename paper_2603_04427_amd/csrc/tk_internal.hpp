@@ -48,6 +48,15 @@ DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV);
 tk_status launch_decode(const DecodeParams& p, int R, int DV, int HG, int key_format, bool paged,
                         hipStream_t stream);
 
+// The library's own decode scratch, for callers that cannot allocate: one fixed
+// device array per GPU (kDecodeScratchBytes), its counter region zeroed once.
+// Every split plan fits: a split context needs fewer than 512 (sequence, head
+// group, split) triples of at most 8 heads, 4096 partial rows of DV + 2 floats.
+constexpr size_t kDecodeScratchBytes = size_t(4) << 20;
+// Device address of the current device's copy (looked up and cleared on the
+// first call on that device, on `stream`); TK_ERR_HIP if that fails.
+tk_status decode_scratch(hipStream_t stream, void** ptr);
+
 // Cache append: grid-stride over 16-byte row slices of the new tokens.
 struct AppendParams {
     const uint16_t* kn;         // [B, Hkv, T, R] bf16 new key rows

@@ -148,6 +148,34 @@ def test_decode_validation(kw, status):
     assert decode(**kw) == status
 
 
+def decode_noalloc(**kw):
+    a = dict(Q=P, K=P, V=P, O=P, batch=2, H_q=32, H_kv=8, ctx_lens=P, max_ctx=4096, r=32, d_v=128,
+             scale=0.0, k_dtype=tb.TK_BF16, k_scale=None, block_table=None, block_size=0,
+             max_blocks=0, num_blocks=0, stream=None)
+    a.update(kw)
+    return tb.lib().tk_attn_decode_noalloc(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(H_q=30), tb.TK_ERR_INVALID_ARG),
+    (dict(max_ctx=-1), tb.TK_ERR_INVALID_ARG),
+    (dict(k_dtype=tb.TK_FP8_E4M3), tb.TK_ERR_INVALID_ARG),     # fp8 without scales
+    (dict(k_scale=P), tb.TK_ERR_INVALID_ARG),                  # scales without fp8
+    (dict(k_dtype=tb.TK_F32), tb.TK_ERR_UNSUPPORTED),
+    (dict(block_size=256), tb.TK_ERR_INVALID_ARG),             # layout args without a table
+    (dict(block_table=P, block_size=256, max_blocks=8, num_blocks=32), tb.TK_ERR_INVALID_ARG),  # 2048 < ctx
+    (dict(block_table=P, block_size=96, max_blocks=64, num_blocks=256), tb.TK_ERR_UNSUPPORTED),
+    (dict(ctx_lens=None), tb.TK_ERR_INVALID_ARG),
+    (dict(O=P_ODD), tb.TK_ERR_INVALID_ARG),
+    (dict(r=48), tb.TK_ERR_UNSUPPORTED),
+    (dict(batch=0), tb.TK_OK),
+])
+def test_decode_noalloc_validation(kw, status):
+    """The no-allocation decode rejects what tk_attn_decode rejects, on the host,
+    before it looks up its scratch (the first HIP call of that path)."""
+    assert decode_noalloc(**kw) == status
+
+
 def test_workspace_query_is_pure_and_sized():
     ws = tb.tk_attn_decode_workspace_bytes
     a = ws(16, 32, 8, 4096, 128)
