@@ -13,7 +13,10 @@ The JSON line reports, besides the contract fields:
                 8 TB/s, and the HBM traffic per call from rocprofv3 counters
                 when they were taken on the current kernel source;
   cpu_baseline  the fp64 oracle on the host cores, on a bounded sample of the
-                same workload (not an optimisation target);
+                same workload (not an optimisation target), with the CPU model,
+                usable cores and OMP_NUM_THREADS; each secondary workload
+                carries its own (whole decode steps; the whole GPT-2 prefill;
+                64 rows of the 8192-token prefill, extrapolated);
   secondary     the other workloads, each with its own roofline: causal prefill
                 at 8192 tokens (bf16 MFMA), the 131072-token paged decode, the
                 fp8-key and 4-bit-key decodes, and the GPT-2 fp32 prefill;
@@ -240,30 +243,81 @@ def append_result(name, B, Hkv, T, r, dv, kdt, dev, steps, warmup):
     }
 
 
-def cpu_baseline(spec, budget_s: float):
-    """The fp64 oracle on the host cores over whole decode steps of the workload,
-    repeated until the time budget is used (at least once)."""
-    import torch
-    from oracle import oracle
-    from paper_2603_04427_amd import accounting as acc
-    from synth import make_decode
+def host_info():
+    """The host the oracle runs on: CPU model, cores this process may use, OpenMP threads."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    nproc = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    return {"cpu_model": model, "nproc": nproc, "omp_num_threads": os.environ.get("OMP_NUM_THREADS")}
 
-    d = make_decode(spec, device="cpu")
-    nbytes = acc.decode_bytes(spec.lens, spec.h_q, spec.h_kv, spec.r, spec.d_v, spec.k_dtype)
-    keys = oracle.Int4(d["k_logical"]) if spec.k_dtype == "int4" else d["k_logical"]
+
+def _repeat(fn, budget_s: float):
+    """Runs fn until budget_s has passed (at least once); returns (runs, seconds)."""
     reps, t0 = 0, time.perf_counter()
     while True:
-        oracle.decode(d["q"], keys, d["v_logical"], d["ctx_lens"], scale=spec.softmax_scale,
-                      k_scale=d["k_scale_logical"])
+        fn()
         reps += 1
         el = time.perf_counter() - t0
         if el >= budget_s:
-            break
-    del d
+            return reps, el
+
+
+def cpu_baseline(spec, budget_s: float, dev=None):
+    """The fp64 oracle on the host cores, timed on a bounded sample of the workload.
+
+    Decode: whole steps (every sequence and head), inputs drawn on the GPU when one
+    is given and copied to the host once. Prefill: the whole call when it is small
+    (the GPT-2 shape), otherwise the last 64 query rows of sequence 0, all heads
+    (bottom-right aligned, so each row sees its full causal prefix), with the
+    whole call's time extrapolated from the sample's FLOP rate."""
+    import torch
+    from oracle import oracle
+    from paper_2603_04427_amd import accounting as acc
+    from synth import make_decode, make_prefill
+
+    info = {"cores": oracle.max_threads(), "kind": "oracle", **host_info()}
+    if hasattr(spec, "ctx"):
+        d = make_decode(spec, device=dev if dev is not None else "cpu")
+        q, v, lens = d["q"].cpu(), d["v_logical"].cpu(), d["ctx_lens"].cpu()
+        k = d["k_logical"].cpu()
+        ks = None if d["k_scale_logical"] is None else d["k_scale_logical"].cpu()
+        del d
+        torch.cuda.empty_cache() if torch.cuda.is_available() else None
+        keys = oracle.Int4(k) if spec.k_dtype == "int4" else k
+        nbytes = acc.decode_bytes(spec.lens, spec.h_q, spec.h_kv, spec.r, spec.d_v, spec.k_dtype,
+                                  spec.blocks_per_seq if spec.paged else None)
+        reps, el = _repeat(lambda: oracle.decode(q, keys, v, lens, scale=spec.softmax_scale, k_scale=ks), budget_s)
+        del q, k, v, keys
+        return {"value": round(nbytes * reps / el / 1e9, 3), "unit": "GB/s", **info,
+                "sample": f"{reps} whole decode steps of {spec.name} (fp64 C oracle, OpenMP, on the contiguous "
+                          f"logical cache), {el:.1f} s", "seconds_per_step": round(el / reps, 4)}
+    p = make_prefill(spec, device=dev if dev is not None else "cpu")
+    whole = spec.batch * spec.h_q * spec.seq_q * spec.seq_k <= (1 << 26)
+    if whole:
+        q, kk, vv = p["q"].cpu(), p["k"].cpu(), p["v"].cpu()
+        flops = acc.prefill_flops(spec.batch, spec.h_q, spec.seq_q, spec.seq_k, spec.r, spec.d_v, spec.causal)
+        what = f"the whole {spec.name} call"
+    else:
+        n = 64
+        q, kk, vv = p["q"][:1, :, -n:].cpu(), p["k"][:1].cpu(), p["v"][:1].cpu()
+        flops = acc.prefill_flops(1, spec.h_q, n, spec.seq_k, spec.r, spec.d_v, spec.causal)
+        what = f"the last {n} query rows of sequence 0 of {spec.name}, all {spec.h_q} heads"
+    del p
     torch.cuda.empty_cache() if torch.cuda.is_available() else None
-    return {"value": round(nbytes * reps / el / 1e9, 3), "unit": "GB/s", "cores": oracle.max_threads(),
-            "kind": "oracle", "sample": f"{reps} full decode steps of {spec.name} (fp64 C oracle, OpenMP), "
-                                        f"{el:.1f} s", "seconds_per_step": round(el / reps, 4)}
+    reps, el = _repeat(lambda: oracle.prefill(q, kk, vv, causal=spec.causal, scale=spec.softmax_scale), budget_s)
+    rate = flops * reps / el
+    full = acc.prefill_flops(spec.batch, spec.h_q, spec.seq_q, spec.seq_k, spec.r, spec.d_v, spec.causal)
+    return {"value": round(rate / 1e12, 6), "unit": "TFLOP/s", **info,
+            "sample": f"{reps} runs of {what} (fp64 C oracle, OpenMP), {el:.1f} s",
+            "seconds_per_step": round(full / rate, 3),
+            "seconds_per_step_is": "measured" if whole else "extrapolated from the sample's FLOP rate"}
 
 
 def copy_calibration(mib: int, dev):
@@ -432,9 +486,13 @@ def main():
                     "seq": spec.seq_q, "r": spec.r, "d_v": spec.d_v, "causal": spec.causal}),
         "roofline": m["roofline"],
     }
-    if not args.no_cpu_baseline and is_decode:
-        print("bench: oracle on the host cores", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(spec, args.cpu_seconds)
+    if not args.no_cpu_baseline:
+        print(f"bench: oracle on the host cores ({main_name})", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(spec, args.cpu_seconds, dev)
+        for n in order:
+            if n != main_name:
+                print(f"bench: oracle on the host cores ({n})", file=sys.stderr, flush=True)
+                results[n]["cpu_baseline"] = cpu_baseline(workloads[n], args.cpu_seconds / 2, dev)
     line["secondary"] = [results[n] for n in order if n != main_name]
     if fullkey:
         line["fullkey_control"] = fullkey

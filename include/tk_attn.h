@@ -13,7 +13,8 @@
  *
  * Conventions shared by all entry points
  *  - Every tensor pointer is a DEVICE pointer owned by the caller; the library
- *    never allocates, frees or synchronises, and keeps no state between calls.
+ *    never allocates, frees or synchronises, and keeps no state between calls,
+ *    except for the fixed per-GPU scratch array behind tk_attn_decode_noalloc.
  *  - Layouts are dense and head-major (innermost dimension last), in elements.
  *  - Query head h reads KV head g = h / (H_q / H_kv) (grouped-query attention;
  *    the Mistral-7B setting of Sec. 3, Exp. 8 has 32 query heads over 8 KV heads).
