@@ -27,6 +27,10 @@ The JSON line reports, besides the contract fields:
   prefill_backward  the backward pass (dQ, dK, dV) of the 8192-token prefill,
                 thin keys and the full-key control, against the bf16 MFMA peak
                 with the algorithmic FLOPs 2 (3r + 2 d_v) per visible pair;
+  thin_projection  the three projections of a layer converted to thin keys
+                (q' = x W_Q', k' = x W_K', v = x W_V, tk_project_heads) at the
+                Mistral 8192-token and GPT-2 1024-token shapes, against the bf16
+                MFMA peak;
   device        the part's CU count, architecture and engine clock levels, and
                 the rates of torch's sum over 2 GiB and copy of 1 GiB on it
                 (context for the fractions of the published peaks);
@@ -203,6 +207,46 @@ def backward_result(name, spec, dev, steps, warmup):
                      "frac": round(achieved / peak, 4), "traffic": traffic_for(name, "prefill_bwd"),
                      "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5),
                      "kernels": "bwd_dq_kernel + bwd_dkdv_kernel"},
+    }
+
+
+PROJECTION_CASES = {  # (B, S, d_model, h_q, h_kv, r, d_v): a converted layer's three projections
+    "thin_projection_mistral_s8192": (4, 8192, 4096, 32, 8, 32, 128),
+    "thin_projection_gpt2_s1024": (1, 1024, 768, 12, 12, 16, 64),
+}
+
+
+def projection_result(name, B, S, d_model, h_q, h_kv, r, dv, dev, steps, warmup):
+    """q' = x W_Q', k' = x W_K' and v = x W_V of a layer converted to thin keys:
+    three tk_project_heads calls per step, random bf16 weights of the converted shapes."""
+    import torch
+    from paper_2603_04427_amd import accounting as acc
+    from paper_2603_04427_amd import prepare_project_heads
+    from synth import normal, stream_key
+
+    x = normal(stream_key(21, 0), B * S * d_model, device=dev).view(B, S, d_model).to(torch.bfloat16)
+    calls, cols = [], 0
+    for t, (n, w) in enumerate(((h_q, r), (h_kv, r), (h_kv, dv))):
+        wt = (normal(stream_key(21, 1 + t), n * w * d_model, device=dev).view(n * w, d_model) *
+              d_model ** -0.5).to(torch.bfloat16)
+        calls.append(prepare_project_heads(x, wt, n))
+        cols += n * w
+
+    def step():
+        for c in calls:
+            c()
+    wall, ev = time_calls([step], steps, warmup)
+    flops = 2 * B * S * d_model * cols
+    achieved = flops / ev / 1e12
+    del x, calls
+    torch.cuda.empty_cache()
+    return {
+        "workload": name, "value": round(flops / wall / 1e12, 2), "unit": "TFLOP/s",
+        "ms_per_call": round(wall * 1e3, 5), "dtype": "bf16",
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": acc.BF16_MFMA_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / acc.BF16_MFMA_PEAK_TFLOPS, 4),
+                     "traffic": None, "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5),
+                     "kernels": "project_kernel x 3 (q', k', v)"},
     }
 
 
@@ -406,6 +450,14 @@ def main():
                           "data": "synthetic", "config": {"workload": args.only}, "roofline": res["roofline"]}),
               flush=True)
         return
+    if args.only and args.only.startswith("thin_projection"):
+        res = projection_result(args.only, *PROJECTION_CASES[args.only], dev, args.steps, min(args.warmup, 5))
+        print(json.dumps({"metric": "thin projection TFLOP/s", "value": res["value"], "unit": "TFLOP/s",
+                          "n_gpus": 1, "steps": args.steps, "warmup": min(args.warmup, 5),
+                          "ms_per_step": res["ms_per_call"], "higher_is_better": True, "scaling": "weak",
+                          "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+                          "config": {"workload": args.only}, "roofline": res["roofline"]}), flush=True)
+        return
     if args.only and args.only.endswith("_backward"):
         spec = workloads[args.only[:-len("_backward")]]
         res = backward_result(args.only, spec, dev, args.steps, min(args.warmup, 3))
@@ -469,6 +521,11 @@ def main():
             print(f"bench: timing {name}", file=sys.stderr, flush=True)
             appends.append(append_result(name, B, 8, T, 32, 128, kdt, dev, max(10, args.steps // 10),
                                          args.warmup))
+    projections = []
+    if not (args.only or args.no_secondary):
+        for name, shape in PROJECTION_CASES.items():
+            print(f"bench: timing {name}", file=sys.stderr, flush=True)
+            projections.append(projection_result(name, *shape, dev, max(10, args.steps // 10), min(args.warmup, 5)))
     m = results[main_name]
     spec = workloads[main_name]
     is_decode = hasattr(spec, "ctx")
@@ -500,6 +557,8 @@ def main():
         line["prefill_backward"] = backward
     if appends:
         line["cache_append"] = appends
+    if projections:
+        line["thin_projection"] = projections
     line["device"] = device_context(dev)
     print(json.dumps(line), flush=True)
 

@@ -243,6 +243,28 @@ tk_status tk_cache_append(const void* K_new, const void* V_new, int batch, int H
                           const int32_t* block_table, int block_size, int max_blocks_per_seq,
                           int num_blocks, hipStream_t stream);
 
+/*
+ * One projection of a layer converted to thin keys (Sec. 2.3, Eq. 6-7), written
+ * head-major for the attention calls above:
+ *
+ *     Y[b, h, s, :] = X[b, s, :] W[:, h * width .. (h + 1) * width - 1]
+ *
+ * After the key projection of every KV head is factored as W_K ~= A B (a
+ * truncated SVD) and B is absorbed into the query projection, a layer needs
+ * the absorbed queries q' = x W_Q' and the thin keys k' = x A (width r each),
+ * and its unchanged values v = x W_V (width d_v): three calls of this function.
+ *
+ *   X  [batch, seq, d_model] bf16: the layer's input rows (hidden states)
+ *   Wt [n_heads * width, d_model] bf16: W transposed (row n is column n of W)
+ *   Y  [batch, n_heads, seq, width] bf16 (the Q / K / V layout of
+ *       tk_attn_prefill and the K_new / V_new layout of tk_cache_append)
+ * Products on the bf16 matrix cores, fp32 accumulation, one round-to-nearest-
+ * even to bf16. Supported: d_model % 8 == 0, width % 4 == 0; pointers 16-byte
+ * aligned. batch == 0 or seq == 0 is a no-op.
+ */
+tk_status tk_project_heads(const void* X, const void* Wt, void* Y, int batch, int seq, int d_model,
+                           int n_heads, int width, hipStream_t stream);
+
 /* A static, human-readable name for a status code. Never NULL. */
 const char* tk_status_str(tk_status status);
 

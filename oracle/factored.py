@@ -46,3 +46,16 @@ def thin_projections(x: np.ndarray, w_q_heads, w_k_heads, r: int, group: int = 1
         sv.append(s)
     qs = [x @ absorb_query(w_q, bs[h // group]) for h, w_q in enumerate(w_q_heads)]
     return np.stack(qs), np.stack(ks), sv
+
+
+def project_heads(x: np.ndarray, w: np.ndarray, n_heads: int) -> np.ndarray:
+    """One projection of a layer, head-major, in fp64: x [B, S, d_model] and
+    w [d_model, n_heads * width] give Y [B, n_heads, S, width] with
+    Y[b, h, s, :] = x[b, s, :] w[:, h width : (h + 1) width] (the layout the
+    attention calls take). The product is numpy's fp64 matmul."""
+    x = np.asarray(x, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    B, S, d_model = x.shape
+    width = w.shape[1] // n_heads
+    y = x.reshape(B * S, d_model) @ w
+    return y.reshape(B, S, n_heads, width).transpose(0, 2, 1, 3).copy()

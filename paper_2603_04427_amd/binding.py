@@ -33,6 +33,7 @@ SIGNATURES = {
     "tk_attn_decode_noalloc": ([_vp, _vp, _vp, _vp, _i, _i, _i, _vp, _i, _i, _i, _f, _i, _vp, _vp, _i, _i, _i,
                                 _vp], _i),
     "tk_cache_append": ([_vp, _vp, _i, _i, _i, _i, _i, _vp, _vp, _vp, _i, _i, _vp, _vp, _i, _i, _i, _vp], _i),
+    "tk_project_heads": ([_vp, _vp, _vp, _i, _i, _i, _i, _i, _vp], _i),
     "tk_status_str": ([_i], ctypes.c_char_p),
     "tk_version": ([], _i),
 }
@@ -369,3 +370,30 @@ def tk_cache_append(K_new: torch.Tensor, V_new: torch.Tensor, positions: torch.T
                     block_table: Optional[torch.Tensor] = None, block_size: int = 0, stream=None) -> None:
     """Write T new tokens per sequence into the cache at positions[b] + t (see include/tk_attn.h)."""
     prepare_cache_append(K_new, V_new, positions, K_cache, V_cache, k_scale, block_table, block_size, stream)()
+
+
+def prepare_project_heads(X: torch.Tensor, Wt: torch.Tensor, n_heads: int, Y: Optional[torch.Tensor] = None,
+                          stream=None) -> PreparedCall:
+    """One thin projection, marshalled: X [B, S, d_model] bf16, Wt [n_heads * width, d_model] bf16
+    (the weight transposed) -> Y [B, n_heads, S, width] bf16."""
+    _check(X, "X", (torch.bfloat16,), 3)
+    _check(Wt, "Wt", (torch.bfloat16,), 2)
+    B, S, d_model = X.shape
+    if Wt.shape[1] != d_model:
+        raise ValueError(f"Wt {tuple(Wt.shape)} does not match d_model {d_model}")
+    if n_heads <= 0 or Wt.shape[0] % n_heads:
+        raise ValueError(f"{Wt.shape[0]} weight rows do not split into {n_heads} heads")
+    width = Wt.shape[0] // n_heads
+    if Y is None:
+        Y = torch.empty(B, n_heads, S, width, dtype=torch.bfloat16, device=X.device)
+    _check(Y, "Y", (torch.bfloat16,), 4)
+    if tuple(Y.shape) != (B, n_heads, S, width):
+        raise ValueError(f"Y must be {(B, n_heads, S, width)}")
+    args = (_ptr(X), _ptr(Wt), _ptr(Y), B, S, d_model, n_heads, width, _stream(stream))
+    return PreparedCall("tk_project_heads", args, (X, Wt, Y))
+
+
+def tk_project_heads(X: torch.Tensor, Wt: torch.Tensor, n_heads: int, Y: Optional[torch.Tensor] = None,
+                     stream=None) -> torch.Tensor:
+    """Y[b, h, s, :] = X[b, s, :] @ Wt[h * width:(h + 1) * width, :].T, head-major bf16."""
+    return prepare_project_heads(X, Wt, n_heads, Y, stream)()

@@ -240,6 +240,29 @@ tk_status tk_attn_decode_noalloc(const void* Q, const void* K_cache, const void*
                        block_table, block_size, max_blocks_per_seq, num_blocks, nullptr, 0, true, stream);
 }
 
+tk_status tk_project_heads(const void* X, const void* Wt, void* Y, int batch, int seq, int d_model, int n_heads,
+                           int width, hipStream_t stream) {
+    if (batch < 0 || seq < 0 || d_model <= 0 || n_heads <= 0 || width <= 0) return TK_ERR_INVALID_ARG;
+    if (batch == 0 || seq == 0) return TK_OK;
+    if (!X || !Wt || !Y) return TK_ERR_INVALID_ARG;
+    if (!aligned16(X) || !aligned16(Wt) || !aligned16(Y)) return TK_ERR_INVALID_ARG;
+    if (d_model % 8 != 0 || width % 4 != 0) return TK_ERR_UNSUPPORTED;
+    const long M = (long)batch * seq, N = (long)n_heads * width;
+    if (M > 0x7fffffffL || N > 0x7fffffffL || tk::project_tiles(M, N) > 0x7fffffffL - 8) return TK_ERR_UNSUPPORTED;
+    tk::ProjectParams p{};
+    p.x = X;
+    p.wt = Wt;
+    p.y = Y;
+    p.M = (int)M;
+    p.N = (int)N;
+    p.K = d_model;
+    p.S = seq;
+    p.heads = n_heads;
+    p.width = width;
+    p.tiles = (int)tk::project_tiles(M, N);
+    return tk::launch_project(p, stream);
+}
+
 tk_status tk_cache_append(const void* K_new, const void* V_new, int batch, int H_kv, int n_new, int r, int d_v,
                           const int32_t* positions, void* K_cache, void* V_cache, int max_ctx, tk_dtype k_dtype,
                           float* k_scale, const int32_t* block_table, int block_size, int max_blocks_per_seq,

@@ -105,6 +105,19 @@ struct PrefillBwdParams {
 
 tk_status launch_prefill_backward(const PrefillBwdParams& p, int R, int DV, hipStream_t stream);
 
+// Thin projection: Y[b, h, s, w] = sum_k X[b, s, k] Wt[h * width + w, k] (bf16
+// in, fp32 accumulation, bf16 out).
+struct ProjectParams {
+    const void* x;   // [M = batch * S, K] bf16 token rows
+    const void* wt;  // [N = heads * width, K] bf16, the weight's columns as rows
+    void* y;         // [batch, heads, S, width] bf16
+    int M, N, K, S, heads, width;
+    int tiles;       // 128 x 128 output tiles
+};
+
+long project_tiles(long M, long N);
+tk_status launch_project(const ProjectParams& p, hipStream_t stream);
+
 tk_status launch_prefill_bf16(const PrefillParams& p, int R, int DV, hipStream_t stream);
 tk_status launch_prefill_f32(const PrefillParams& p, int R, int DV, hipStream_t stream);
 

@@ -12,16 +12,18 @@ The factorisation is per KV head (the per-head key widths of the paper's
 tables, and the grouping of GQA); the query heads of a group share its factor.
 Values and the output projection are untouched: V keeps its full width.
 
-This is weight preprocessing, done once on the host before serving; it is not
-a step of the attention path. `project_thin` applies the converted projections
-with library matrix products to produce the head-major bf16 Q, K and V that
-`tk_attn_prefill` and `tk_cache_append` take. The softmax scale that preserves
+The factorisation is weight preprocessing, done once on the host before
+serving. `project_thin` applies the converted projections on the GPU with the
+library's projection kernel (tk_project_heads) to produce the head-major bf16
+Q, K and V that `tk_attn_prefill` and `tk_cache_append` take. The softmax scale that preserves
 a pretrained model's attention is the original 1/sqrt(d_head), passed to the
 kernels explicitly.
 """
 from __future__ import annotations
 
 import torch
+
+from .binding import tk_project_heads
 
 
 def _head_blocks(w: torch.Tensor, n_heads: int) -> torch.Tensor:
@@ -70,17 +72,26 @@ def logit_error_bound(x_q: torch.Tensor, w_q: torch.Tensor, x_k: torch.Tensor, s
     return qn[:, None] * sigma_next * kn[None, :]
 
 
+def transposed_bf16(w: torch.Tensor, device) -> torch.Tensor:
+    """A projection weight w [d_model, n_heads * width] as the kernel takes it:
+    transposed, [n_heads * width, d_model], bf16, contiguous, on ``device``
+    (done once per layer, with the conversion)."""
+    return w.detach().t().to(device=device, dtype=torch.bfloat16).contiguous()
+
+
 def project_thin(x: torch.Tensor, w_q_thin: torch.Tensor, w_k_thin: torch.Tensor, w_v: torch.Tensor,
-                 h_q: int, h_kv: int, dtype: torch.dtype = torch.bfloat16):
+                 h_q: int, h_kv: int):
     """Queries, thin keys and values of hidden states x [B, S, d_model], head-major
-    and contiguous in `dtype` on x's device: Q [B, h_q, S, r], K [B, h_kv, S, r],
-    V [B, h_kv, S, d_v]. The products are library matrix multiplications in
-    float32; the results are rounded once to `dtype`."""
-    B, S, d_model = x.shape
-    xs = x.to(torch.float32)
+    bf16 on x's device: Q [B, h_q, S, r], K [B, h_kv, S, r], V [B, h_kv, S, d_v].
+
+    Each projection is one tk_project_heads call (bf16 matrix cores, fp32
+    accumulation, one rounding to bf16) on the weights as ``factor_layer``
+    returns them, [d_model, n * width], converted with ``transposed_bf16``
+    (a serving loop converts once and calls tk_project_heads directly); x is
+    taken in bf16."""
+    xb = x.to(torch.bfloat16).contiguous()
 
     def heads(w, n):
-        y = torch.matmul(xs, w.to(device=x.device, dtype=torch.float32))  # [B, S, n * width]
-        return y.reshape(B, S, n, -1).permute(0, 2, 1, 3).contiguous().to(dtype)
+        return tk_project_heads(xb, transposed_bf16(w, x.device), n)
 
     return heads(w_q_thin, h_q), heads(w_k_thin, h_kv), heads(w_v, h_kv)

@@ -102,17 +102,32 @@ def test_logits_match_the_oracle_factorisation(h_q, h_kv, r):
     assert torch.allclose(sigma, torch.from_numpy(__import__("numpy").stack(so)), rtol=1e-12, atol=1e-12)
 
 
-def test_project_thin_is_head_major():
-    B, S, d_model, h_q, h_kv, r, d_v = 2, 7, 32, 4, 2, 8, 16
-    x = draw(8, B, S, d_model).to(torch.float32)
-    w_q = draw(9, d_model, h_q * r).to(torch.float32)
-    w_k = draw(10, d_model, h_kv * r).to(torch.float32)
-    w_v = draw(11, d_model, h_kv * d_v).to(torch.float32)
-    q, k, v = factor.project_thin(x, w_q, w_k, w_v, h_q, h_kv, dtype=torch.float32)
-    assert q.shape == (B, h_q, S, r) and k.shape == (B, h_kv, S, r) and v.shape == (B, h_kv, S, d_v)
-    assert q.is_contiguous() and k.is_contiguous() and v.is_contiguous()
-    assert torch.allclose(q[1, 3, 5], x[1, 5] @ w_q[:, 3 * r:4 * r], rtol=1e-5, atol=1e-5)
-    assert torch.allclose(v[0, 1, 2], x[0, 2] @ w_v[:, d_v:2 * d_v], rtol=1e-5, atol=1e-5)
+def test_transposed_weights_layout():
+    """The projection kernel takes each weight transposed ([n_heads * width, d_model])
+    in bf16: entry (n, k) is w[k, n] rounded once."""
+    w = draw(9, 32, 4 * 8).to(torch.float32)
+    wt = factor.transposed_bf16(w, "cpu")
+    assert wt.shape == (32, 32) and wt.dtype == torch.bfloat16 and wt.is_contiguous()
+    for n, k in ((0, 0), (5, 17), (31, 3), (12, 31)):
+        assert wt[n, k].item() == w[k, n].to(torch.bfloat16).item()
+
+
+def test_oracle_projection_is_head_major():
+    """oracle.factored.project_heads against explicit loops (pure Python sums) on a
+    tiny input: Y[b, h, s, w] = sum_k X[b, s, k] W[k, h * width + w]."""
+    import numpy as np
+    B, S, d_model, heads, width = 2, 3, 5, 2, 4
+    x = draw(12, B, S, d_model).numpy()
+    w = draw(13, d_model, heads * width).numpy()
+    y = factored.project_heads(x, w, heads)
+    assert y.shape == (B, heads, S, width)
+    for b in range(B):
+        for h in range(heads):
+            for s_ in range(S):
+                for c in range(width):
+                    want = math.fsum(float(x[b, s_, k]) * float(w[k, h * width + c]) for k in range(d_model))
+                    assert abs(y[b, h, s_, c] - want) <= 1e-13 * (1 + abs(want))
+    assert np.array_equal(factored.project_heads(x[:, :0], w, heads), np.zeros((B, heads, 0, width)))
 
 
 def test_bad_arguments_are_rejected():
