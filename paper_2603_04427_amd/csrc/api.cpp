@@ -246,7 +246,7 @@ tk_status tk_project_heads(const void* X, const void* Wt, void* Y, int batch, in
     if (batch == 0 || seq == 0) return TK_OK;
     if (!X || !Wt || !Y) return TK_ERR_INVALID_ARG;
     if (!aligned16(X) || !aligned16(Wt) || !aligned16(Y)) return TK_ERR_INVALID_ARG;
-    if (d_model % 8 != 0 || width % 4 != 0) return TK_ERR_UNSUPPORTED;
+    if (d_model % 32 != 0 || width % 4 != 0) return TK_ERR_UNSUPPORTED;
     const long M = (long)batch * seq, N = (long)n_heads * width;
     if (M > 0x7fffffffL || N > 0x7fffffffL || tk::project_tiles(M, N) > 0x7fffffffL - 8) return TK_ERR_UNSUPPORTED;
     tk::ProjectParams p{};

@@ -13,7 +13,7 @@
 //
 // The weight is passed transposed, Wt [n_heads * width, d_model] (one row per
 // output column), so both operands of the product are contiguous along
-// d_model. The tile computes C^T = Wt X^T: a lane of each 32x32 accumulator
+// d_model, which must be a multiple of 32 (one k-tile). The tile computes C^T = Wt X^T: a lane of each 32x32 accumulator
 // then holds four consecutive output columns of one token, which become one
 // 8-byte store into the head-major output row.
 #include "tk_device.hpp"
@@ -23,29 +23,55 @@ namespace tk {
 
 namespace {
 
-constexpr int kPBM = 128;  // tokens per workgroup tile
-constexpr int kPBN = 128;  // output columns per workgroup tile
-constexpr int kPBK = 64;   // d_model per k-tile (8 chunks of 8 bf16 per row)
-constexpr int kPThreads = 256;
+constexpr int kPBK = 32;   // d_model per k-tile: 4 chunks of 8 bf16 per row
+constexpr int kStages = 3; // k-tiles in LDS: the one multiplied and two in flight
 constexpr int kXcdCount = 8;
-constexpr int kChunks = kPBM * kPBK / 8;  // 16-byte chunks of one operand tile (= kPBN * kPBK / 8)
-constexpr int kPerThread = kChunks / kPThreads;
-static_assert(kPBM == kPBN, "both operand tiles have the same shape");
 
-struct ProjSmem {
-    uint16_t w[2][kPBN * kPBK];  // Wt rows of the tile, XOR-swizzled 16-byte chunks
-    uint16_t x[2][kPBM * kPBK];  // token rows of the tile, same swizzle
+// A workgroup tile of BN output columns (weight rows) x BM tokens. Its waves are
+// laid out (BN / 64) x 2: each owns 64 columns x BM / 2 tokens.
+template <int BN, int BM>
+struct ProjTile {
+    static constexpr int kWaves = (BN / 64) * 2;
+    static constexpr int kThreads = 64 * kWaves;
+    static constexpr int kMB = BM / 64;                         // 32-token blocks per wave
+    static constexpr int kWCopies = BN * kPBK / 8 / kThreads;  // copies per lane and k-tile
+    static constexpr int kXCopies = BM * kPBK / 8 / kThreads;
+    static constexpr int kCopies = kWCopies + kXCopies;        // a lane's copies in flight per k-tile
+    static_assert(kWCopies * kThreads * 8 == BN * kPBK && kXCopies * kThreads * 8 == BM * kPBK, "tiling");
+    uint16_t w[kStages][BN * kPBK];  // weight rows of the tile (swizzled 16-byte chunks)
+    uint16_t x[kStages][BM * kPBK];  // token rows of the tile (same swizzle)
 };
 
-// element offset of chunk kc (0..7) of tile row r: chunks rotate by row so that
-// the 32 rows one matrix-operand read touches spread over all LDS banks
-__device__ __forceinline__ int sw(int r, int kc) { return r * kPBK + ((kc ^ (r & 7)) << 3); }
+// Chunk kc (0..3) of tile row r sits in slot 4 r + (kc ^ ((r / 2) % 4)). Rows are
+// 64 bytes, so two rows share one 128-byte bank period; the rotation makes the
+// same chunk of any 8 consecutive rows cover all 32 banks. The map is its own
+// inverse: slot 4 r + q holds chunk q ^ ((r / 2) % 4).
+__device__ __forceinline__ int sw(int r, int kc) { return r * kPBK + ((kc ^ ((r >> 1) & 3)) << 3); }
 
-__global__ __launch_bounds__(kPThreads, 2) void project_kernel(const ProjectParams p) {
-    __shared__ ProjSmem sm;
+template <int N>
+__device__ __forceinline__ void wait_copies(bool next_in_flight) {
+    if (next_in_flight)
+        asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+    else
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// Each wave multiplies a 64-column x BM / 2-token block: per 16-wide k-step 2
+// weight and BM / 64 token operand reads from LDS feed 2 BM / 64 MFMAs. Tiles
+// come from HBM by global->LDS copies (no staging registers), issued two
+// k-tiles ahead into a three-stage ring.
+template <int BN>
+constexpr int proj_threads() { return 64 * (BN / 64) * 2; }
+
+template <int BN, int BM>
+__global__ __launch_bounds__(proj_threads<BN>(), 1) void project_kernel(const ProjectParams p) {
+    using T = ProjTile<BN, BM>;
+    constexpr int kPThreads = T::kThreads, kWCopies = T::kWCopies, kXCopies = T::kXCopies;
+    constexpr int kPBN = BN, kPBM = BM;
+    __shared__ T sm;
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wn = wave >> 1, wm = wave & 1;  // this wave's 64x64 quarter of the tile
+    const int wn = wave >> 1, wm = wave & 1;  // (BN / 64) x 2 waves over the tile's columns x tokens
     // XCD-aware order: workgroups are dealt to the 8 XCDs round-robin; each XCD
     // takes a contiguous range of tiles, column tiles fastest, so the column
     // tiles of one token tile run on one XCD and share its rows through its L2
@@ -56,83 +82,79 @@ __global__ __launch_bounds__(kPThreads, 2) void project_kernel(const ProjectPara
     const int n_base = (logical % n_tiles) * kPBN, m_base = (logical / n_tiles) * kPBM;
     const int col = lane & 31, half = lane >> 5;
 
-    // chunk (row, kc) of each operand this thread stages, as byte offsets; rows
-    // outside the matrix load zeros
-    const uint16_t* wsrc[kPerThread];
-    const uint16_t* xsrc[kPerThread];
-    bool wok[kPerThread], xok[kPerThread];
-    int soff[kPerThread];
+    // Copy i of this lane fills LDS slot i * 256 + tid of the tile: row slot / 4,
+    // chunk (slot % 4) ^ ((row / 2) % 4) of that row in the matrix. Rows past the
+    // matrix re-read its last row (finite values whose outputs are not stored).
+    const int wlast = (p.N - n_base < kPBN ? p.N - n_base : kPBN) - 1;
+    const int xlast = (p.M - m_base < kPBM ? p.M - m_base : kPBM) - 1;
+    uint32_t woff[kWCopies], xoff[kXCopies];
 #pragma unroll
-    for (int i = 0; i < kPerThread; ++i) {
-        const int c = tid + i * kPThreads, r = c >> 3, kc = c & 7;
-        soff[i] = sw(r, kc);
-        wok[i] = n_base + r < p.N;
-        xok[i] = m_base + r < p.M;
-        wsrc[i] = (const uint16_t*)p.wt + (size_t)(wok[i] ? n_base + r : 0) * p.K + kc * 8;
-        xsrc[i] = (const uint16_t*)p.x + (size_t)(xok[i] ? m_base + r : 0) * p.K + kc * 8;
+    for (int i = 0; i < kWCopies; ++i) {
+        const int slot = i * kPThreads + tid, r = slot >> 2, kc = (slot & 3) ^ ((r >> 1) & 3);
+        woff[i] = (uint32_t)(((r < wlast ? r : wlast) * p.K + kc * 8) * 2);
     }
-    uint4 wreg[kPerThread], xreg[kPerThread];
-    auto load = [&](int k0) {
 #pragma unroll
-        for (int i = 0; i < kPerThread; ++i) {
-            const int kk = k0 + (((tid + i * kPThreads) & 7) << 3);
-            wreg[i] = (wok[i] && kk < p.K) ? *(const uint4*)(wsrc[i] + k0) : make_uint4(0, 0, 0, 0);
-            xreg[i] = (xok[i] && kk < p.K) ? *(const uint4*)(xsrc[i] + k0) : make_uint4(0, 0, 0, 0);
-        }
-    };
-    auto stash = [&](int buf) {
+    for (int i = 0; i < kXCopies; ++i) {
+        const int slot = i * kPThreads + tid, r = slot >> 2, kc = (slot & 3) ^ ((r >> 1) & 3);
+        xoff[i] = (uint32_t)(((r < xlast ? r : xlast) * p.K + kc * 8) * 2);
+    }
+    const char* wg = (const char*)((const uint16_t*)p.wt + (size_t)n_base * p.K);
+    const char* xg = (const char*)((const uint16_t*)p.x + (size_t)m_base * p.K);
+    auto issue = [&](int kt, int stage) {
+        const char* wk = wg + (size_t)kt * kPBK * 2;
+        const char* xk = xg + (size_t)kt * kPBK * 2;
 #pragma unroll
-        for (int i = 0; i < kPerThread; ++i) {
-            *(uint4*)(sm.w[buf] + soff[i]) = wreg[i];
-            *(uint4*)(sm.x[buf] + soff[i]) = xreg[i];
-        }
+        for (int i = 0; i < kWCopies; ++i) copy16_to_lds(wk, woff[i], sm.w[stage] + (i * kPThreads + wave * 64) * 8);
+#pragma unroll
+        for (int i = 0; i < kXCopies; ++i) copy16_to_lds(xk, xoff[i], sm.x[stage] + (i * kPThreads + wave * 64) * 8);
     };
 
-    f32x16 acc[2][2];
+    f32x16 acc[2][T::kMB];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < T::kMB; ++j)
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    const int nk = (p.K + kPBK - 1) / kPBK;
-    load(0);
-    stash(0);
-    __syncthreads();
+    const int nk = p.K / kPBK;
+    issue(0, 0);
+    if (nk > 1) issue(1, 1);
+    wait_copies<T::kCopies>(nk > 1);  // this lane's copies of k-tile 0 have landed
+    __syncthreads();      // ... and everyone's
+    int stage = 0;
     for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) load((kt + 1) * kPBK);
+        // the stage k-tile kt + 2 goes to was last read in iteration kt - 1, which
+        // every wave has finished (the barrier at its end)
+        const bool ahead = kt + 2 < nk;
+        if (ahead) issue(kt + 2, stage == 0 ? 2 : stage - 1);
+        const uint16_t* ws = sm.w[stage];
+        const uint16_t* xs = sm.x[stage];
 #pragma unroll
         for (int ks = 0; ks < kPBK / 16; ++ks) {
             const int kc = 2 * ks + half;
-            bf16x8 a[2], b[2];
+            bf16x8 a[2], b[T::kMB];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                const int r = wn * 64 + i * 32 + col;
-                a[i] = *(const bf16x8*)(sm.w[buf] + sw(r, kc));
-            }
+            for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(ws + sw(wn * 64 + i * 32 + col, kc));
 #pragma unroll
-            for (int j = 0; j < 2; ++j) {
-                const int r = wm * 64 + j * 32 + col;
-                b[j] = *(const bf16x8*)(sm.x[buf] + sw(r, kc));
-            }
+            for (int j = 0; j < T::kMB; ++j) b[j] = *(const bf16x8*)(xs + sw(wm * (BM / 2) + j * 32 + col, kc));
 #pragma unroll
             for (int i = 0; i < 2; ++i)
 #pragma unroll
-                for (int j = 0; j < 2; ++j)
+                for (int j = 0; j < T::kMB; ++j)
                     acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
         }
-        if (kt + 1 < nk) stash(buf ^ 1);
+        if (kt + 1 < nk) wait_copies<T::kCopies>(ahead);  // k-tile kt + 1 has landed (kt + 2 may still fly)
         __syncthreads();
+        stage = stage == kStages - 1 ? 0 : stage + 1;
     }
 
     // ---- epilogue: lane (col, half) of block (i, j) holds output columns
     // n0 + 8 g + 4 half + 0..3 (g = 0..3) of token m0 + col, rounded to bf16 and
     // stored as 8 bytes into Y[b, h, s, w .. w + 3]
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int m = m_base + wm * 64 + j * 32 + col;
+    for (int j = 0; j < T::kMB; ++j) {
+        const int m = m_base + wm * (BM / 2) + j * 32 + col;
         if (m >= p.M) continue;
         const int bb = m / p.S, s = m - bb * p.S;
 #pragma unroll
@@ -153,11 +175,24 @@ __global__ __launch_bounds__(kPThreads, 2) void project_kernel(const ProjectPara
 
 }  // namespace
 
-long project_tiles(long M, long N) { return ((M + kPBM - 1) / kPBM) * ((N + kPBN - 1) / kPBN); }
+// 256 x 256 tiles (8 waves, one workgroup per CU) when they give every CU a
+// tile; otherwise 128 x 128 tiles (4 waves, two workgroups per CU), so that
+// narrow projections (a few KV heads of thin keys) and short sequences still
+// spread over the part.
+static bool big_tiles(long M, long N) { return ((M + 255) / 256) * ((N + 255) / 256) >= 256; }
+
+long project_tiles(long M, long N) {
+    return big_tiles(M, N) ? ((M + 255) / 256) * ((N + 255) / 256) : ((M + 127) / 128) * ((N + 127) / 128);
+}
 
 tk_status launch_project(const ProjectParams& p, hipStream_t st) {
     const long launched = ((long)p.tiles + kXcdCount - 1) / kXcdCount * kXcdCount;
-    hipLaunchKernelGGL(project_kernel, dim3((unsigned)launched), dim3(kPThreads), 0, st, p);
+    if (big_tiles(p.M, p.N))
+        hipLaunchKernelGGL((project_kernel<256, 256>), dim3((unsigned)launched), dim3(ProjTile<256, 256>::kThreads),
+                           0, st, p);
+    else
+        hipLaunchKernelGGL((project_kernel<128, 128>), dim3((unsigned)launched), dim3(ProjTile<128, 128>::kThreads),
+                           0, st, p);
     return hipGetLastError() == hipSuccess ? TK_OK : TK_ERR_HIP;
 }
 

@@ -7,7 +7,8 @@ oracle on the same seeded inputs (Sec. 2.3, Eq. 6-7).
   exact products (at most d_model * 2^-24 of sum |x||w|) and one rounding to
   bf16 (at most 2^-8 of the value):
       |Y_gpu - Y| <= 2^-8 |Y| + (1 + 2^-8) d_model 2^-24 (|X| |W|).
-  Shapes cover tile tails in tokens, columns and d_model, head widths 4-128
+  Shapes cover both tile shapes the kernel picks (128 x 128 and 256 x 256),
+  tile tails in tokens and columns, odd numbers of k-tiles, head widths 4-128
   and a single token.
 * The converted layer: factor.factor_layer on a layer whose key heads have exact
   rank r, then factor.project_thin (three kernel calls) against
@@ -53,7 +54,9 @@ SHAPES = [  # (B, S, d_model, heads, width)
     (2, 300, 1024, 2, 128),   # full-width values of 2 KV heads
     (3, 77, 4096, 32, 32),    # Mistral-7B d_model, 32 query heads of r 32
     (1, 1, 64, 1, 4),         # one token, one narrow head
-    (1, 129, 136, 3, 20),     # d_model not a multiple of the 64-wide k-tile, 60 columns
+    (1, 129, 160, 3, 20),     # an odd number of 32-wide k-tiles, 60 columns, ragged tokens
+    (2, 2048, 1024, 32, 128),  # 256 x 256 workgroup tiles (at least one per CU)
+    (1, 4100, 256, 64, 68),   # 256 x 256 tiles with tails in tokens and columns
 ]
 
 
@@ -83,9 +86,9 @@ def test_empty_and_rejected():
     with pytest.raises(TkError, match="unsupported"):   # width 3 is not a multiple of 4
         tk_project_heads(torch.zeros(1, 4, 64, dtype=torch.bfloat16, device=dev),
                          torch.zeros(6, 64, dtype=torch.bfloat16, device=dev), 2)
-    with pytest.raises(TkError, match="unsupported"):   # d_model 60 is not a multiple of 8
-        tk_project_heads(torch.zeros(1, 4, 60, dtype=torch.bfloat16, device=dev),
-                         torch.zeros(8, 60, dtype=torch.bfloat16, device=dev), 2)
+    with pytest.raises(TkError, match="unsupported"):   # d_model 40 is not a multiple of 32
+        tk_project_heads(torch.zeros(1, 4, 40, dtype=torch.bfloat16, device=dev),
+                         torch.zeros(8, 40, dtype=torch.bfloat16, device=dev), 2)
 
 
 @pytest.mark.parametrize("B,S,d_model,h_q,h_kv,d_head,r", [
