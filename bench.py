@@ -27,6 +27,10 @@ The JSON line reports, besides the contract fields:
   prefill_backward  the backward pass (dQ, dK, dV) of the 8192-token prefill,
                 thin keys and the full-key control, against the bf16 MFMA peak
                 with the algorithmic FLOPs 2 (3r + 2 d_v) per visible pair;
+  decode_batch_sweep  the Mistral-shaped decode (context 4096) at batch 1, 4,
+                8, 16 and 32 (the batch sizes of the paper's decode table), thin
+                keys against standard-width keys, with the time ratio next to
+                the byte ratio of the two caches;
   thin_projection  the three projections of a layer converted to thin keys
                 (q' = x W_Q', k' = x W_K', v = x W_V, tk_project_heads) at the
                 Mistral 8192-token and GPT-2 1024-token shapes, against the bf16
@@ -208,6 +212,38 @@ def backward_result(name, spec, dev, steps, warmup):
                      "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5),
                      "kernels": "bwd_dq_kernel + bwd_dkdv_kernel"},
     }
+
+
+SWEEP_BATCHES = (1, 4, 8, 16, 32)
+
+
+def batch_sweep(dev, steps, warmup, rotate):
+    """Decode at the batch sizes of the paper's decode table (Mistral-7B shape,
+    context 4096): thin keys (r 32) against standard-width keys (r 128, same
+    values), with the ratio of the two times next to the ratio of the bytes
+    the two caches hold (the attention-only form of Eq. 10)."""
+    import torch
+    from dataclasses import replace
+    from paper_2603_04427_amd import accounting as acc
+    from synth import WORKLOADS
+
+    base = WORKLOADS["mistral_decode_b16"]
+    out = []
+    for B in SWEEP_BATCHES:
+        row = {"batch": B}
+        for tag, r in (("thin", 32), ("full", 128)):
+            spec = replace(base, name=f"decode_b{B}_{tag}", batch=B, r=r)
+            calls = decode_setup(spec, dev, rotate)
+            res = decode_result(spec.name, spec, calls, steps, warmup)
+            del calls
+            torch.cuda.empty_cache()
+            row[tag] = {"kernel_ms": res["roofline"]["kernel_ms"], "GBps": res["roofline"]["achieved"],
+                        "frac": res["roofline"]["frac"]}
+        nb = lambda r: acc.decode_bytes((base.ctx,) * B, base.h_q, base.h_kv, r, base.d_v, "bf16")
+        row["thin_key_speedup"] = round(row["full"]["kernel_ms"] / row["thin"]["kernel_ms"], 3)
+        row["byte_ratio"] = round(nb(128) / nb(32), 3)
+        out.append(row)
+    return out
 
 
 PROJECTION_CASES = {  # (B, S, d_model, h_q, h_kv, r, d_v): a converted layer's three projections
@@ -526,6 +562,10 @@ def main():
         for name, shape in PROJECTION_CASES.items():
             print(f"bench: timing {name}", file=sys.stderr, flush=True)
             projections.append(projection_result(name, *shape, dev, max(10, args.steps // 10), min(args.warmup, 5)))
+    sweep = []
+    if not (args.only or args.no_secondary or args.no_fullkey):
+        print("bench: timing the decode batch sweep", file=sys.stderr, flush=True)
+        sweep = batch_sweep(dev, max(20, args.steps // 4), max(20, args.warmup // 10), args.rotate)
     m = results[main_name]
     spec = workloads[main_name]
     is_decode = hasattr(spec, "ctx")
@@ -559,6 +599,8 @@ def main():
         line["cache_append"] = appends
     if projections:
         line["thin_projection"] = projections
+    if sweep:
+        line["decode_batch_sweep"] = sweep
     line["device"] = device_context(dev)
     print(json.dumps(line), flush=True)
 
