@@ -259,8 +259,8 @@ tk_status tk_cache_append(const void* K_new, const void* V_new, int batch, int H
  *   Y  [batch, n_heads, seq, width] bf16 (the Q / K / V layout of
  *       tk_attn_prefill and the K_new / V_new layout of tk_cache_append)
  * Products on the bf16 matrix cores, fp32 accumulation, one round-to-nearest-
- * even to bf16. Supported: d_model % 32 == 0, width % 4 == 0; pointers 16-byte
- * aligned. batch == 0 or seq == 0 is a no-op.
+ * even to bf16. Supported: d_model % 32 == 0 and d_model <= 2^22, width % 4 == 0;
+ * pointers 16-byte aligned. batch == 0 or seq == 0 is a no-op.
  */
 tk_status tk_project_heads(const void* X, const void* Wt, void* Y, int batch, int seq, int d_model,
                            int n_heads, int width, hipStream_t stream);

@@ -247,6 +247,7 @@ tk_status tk_project_heads(const void* X, const void* Wt, void* Y, int batch, in
     if (!X || !Wt || !Y) return TK_ERR_INVALID_ARG;
     if (!aligned16(X) || !aligned16(Wt) || !aligned16(Y)) return TK_ERR_INVALID_ARG;
     if (d_model % 32 != 0 || width % 4 != 0) return TK_ERR_UNSUPPORTED;
+    if (d_model > (1 << 22)) return TK_ERR_UNSUPPORTED;  // 32-bit copy offsets within a 256-row tile
     const long M = (long)batch * seq, N = (long)n_heads * width;
     if (M > 0x7fffffffL || N > 0x7fffffffL || tk::project_tiles(M, N) > 0x7fffffffL - 8) return TK_ERR_UNSUPPORTED;
     tk::ProjectParams p{};

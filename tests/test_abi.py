@@ -176,6 +176,29 @@ def test_decode_noalloc_validation(kw, status):
     assert decode_noalloc(**kw) == status
 
 
+def project(**kw):
+    a = dict(X=P, Wt=P, Y=P, batch=2, seq=128, d_model=1024, n_heads=8, width=32, stream=None)
+    a.update(kw)
+    return tb.lib().tk_project_heads(*a.values())
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(batch=-1), tb.TK_ERR_INVALID_ARG),
+    (dict(d_model=0), tb.TK_ERR_INVALID_ARG),
+    (dict(n_heads=0), tb.TK_ERR_INVALID_ARG),
+    (dict(width=0), tb.TK_ERR_INVALID_ARG),
+    (dict(X=None), tb.TK_ERR_INVALID_ARG),
+    (dict(Y=P_ODD), tb.TK_ERR_INVALID_ARG),
+    (dict(d_model=1000), tb.TK_ERR_UNSUPPORTED),     # not a multiple of 32
+    (dict(width=30), tb.TK_ERR_UNSUPPORTED),         # not a multiple of 4
+    (dict(d_model=1 << 23), tb.TK_ERR_UNSUPPORTED),  # copy offsets would not fit 32 bits
+    (dict(batch=0), tb.TK_OK),
+    (dict(seq=0), tb.TK_OK),
+])
+def test_project_validation(kw, status):
+    assert project(**kw) == status
+
+
 def test_workspace_query_is_pure_and_sized():
     ws = tb.tk_attn_decode_workspace_bytes
     a = ws(16, 32, 8, 4096, 128)
