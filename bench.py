@@ -572,9 +572,10 @@ def main():
     line = {
         "metric": METRIC, "value": m["value"], "unit": m["unit"], "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": m["ms_per_call"], "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "bf16" if (not is_decode or spec.k_dtype == "bf16") else
-        f"{spec.k_dtype}-keys/bf16",
-        "data": "synthetic (seeded N(0,1) draws shaped like the paper's Mistral-7B decode)",
+        "vs_baseline": None, "dtype": (spec.dtype if not is_decode else
+                                       "bf16" if spec.k_dtype == "bf16" else f"{spec.k_dtype}-keys/bf16"),
+        "data": ("synthetic (seeded N(0,1) draws shaped like the paper's Mistral-7B decode)"
+                 if main_name == "mistral_decode_b16" else f"synthetic (seeded N(0,1) draws, workload {main_name})"),
         "config": ({"workload": main_name, "batch": spec.batch, "h_q": spec.h_q, "h_kv": spec.h_kv,
                     "ctx": spec.ctx, "r": spec.r, "d_v": spec.d_v, "k_dtype": spec.k_dtype,
                     "layout": "paged" if spec.paged else "contiguous", "rotate": m.get("rotate")}

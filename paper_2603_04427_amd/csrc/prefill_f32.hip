@@ -10,7 +10,10 @@
 // w, w + 4, ...), each wave with its own tile in LDS and its own online-softmax
 // state; the 4 partial results are merged in LDS with the log-sum-exp rule at
 // the end. Workgroups are ranked by prefix length across heads and sequences,
-// longest first, so the round-robin dispatch deals every XCD the same mix.
+// longest first, so the round-robin dispatch deals every XCD the same mix; every
+// other round of 256 workgroups (one per CU) takes its ranks in reverse, so a CU
+// that received one of the longest blocks in one round receives one of the
+// shorter blocks of the next.
 //
 // Inside a wave: transposed scores S^T = K Q^T per 16-key block, so lane (g, n)
 // of lane group g = lane / 16 serves query n = lane % 16, and O^T = V^T P^T.
@@ -19,12 +22,16 @@
 //    [g R/4, (g+1) R/4) (contiguous in the K row, read 16 bytes at a time);
 //  * the value product takes, in step i of a key block, keys 4 g + i: the keys
 //    whose scores lane group g already holds in accumulator register i, so P^T
-//    is used in place with no repacking. V is stored transposed ([d_v][keys]
-//    fp32, natural key order) so one 16-byte read gives a lane the operands of
-//    four steps.
+//    is used in place with no repacking. V stays in its natural [keys][d_v]
+//    layout in LDS (rows padded by 16 bytes, so the four lane groups' rows fall
+//    on disjoint banks); a lane reads its four keys of one column with two
+//    paired 4-byte reads. A transposed copy would give one 16-byte read instead,
+//    but the transpose has to be done in registers, and the fp32 matrix
+//    instructions do not overlap VALU work, so those moves cost issue time.
 // Row maxima and sums reduce over the four lane groups of a query (lane
 // n, n + 16, n + 32, n + 48). A wave loads its next tile into registers while
-// it computes the current one.
+// it computes the current one; the loads are waited for only when that tile is
+// stored to LDS at the top of the next step.
 #include "tk_device.hpp"
 #include "tk_internal.hpp"
 
@@ -40,71 +47,67 @@ constexpr int kRows = 16;  // query rows per workgroup
 
 // Keys per tile: 32 (two 16-key blocks). A wave's tile then costs 32 (R + DV) / 64
 // floats of prefetch registers per lane, and at the GPT-2 shape (r 16, d_v 64)
-// the workgroup's four tiles take 45 KB of LDS, so three workgroups share a CU
-// and one wave's softmax overlaps another's matrix products (with 64-key tiles
-// only one workgroup fits and a wave's dependent score -> softmax -> value
-// chain leaves its matrix core idle for about 40 % of a tile).
+// the workgroup's four tiles take 44 KB of LDS, so three workgroups share a CU
+// and each SIMD interleaves three waves: while one waits on its dependent
+// score -> softmax -> value chain, another issues matrix products (with 64-key
+// tiles only one workgroup fits and that chain leaves the matrix core idle for
+// about 40 % of a tile).
 template <int R, int DV>
 struct alignas(16) WaveTile {
     static constexpr int BN = 32;
     static constexpr int KB = BN / 32;  // 32-key blocks per tile
     static constexpr int KS = R + 4;    // floats per K row in LDS (16-byte pad)
-    static constexpr int VS = BN + 4;   // floats per transposed V row
+    static constexpr int VS = DV + 4;   // floats per V row in LDS (16-byte pad)
     float k[BN * KS];
-    float vt[DV * VS];
+    float v[BN * VS];
 };
 
-// One tile of one wave in registers: 16-byte K chunks and 4-key x 4-column V quads.
+// One tile of one wave in registers: 16-byte chunks of K rows and of V rows.
 template <int R, int DV>
 struct WaveRegs {
     static constexpr int BN = WaveTile<R, DV>::BN;
     static constexpr int KCH = BN * R / 4;
-    static constexpr int VQ = (BN / 4) * (DV / 4);
-    static_assert(KCH % 64 == 0 && VQ % 64 == 0, "tile does not divide over the lanes");
+    static constexpr int VCH = BN * DV / 4;
+    static_assert(KCH % 64 == 0 && VCH % 64 == 0, "tile does not divide over the lanes");
     static constexpr int KL = KCH / 64;
-    static constexpr int VL = VQ / 64;
+    static constexpr int VL = VCH / 64;
     float4 k[KL];
-    float4 v[VL][4];
+    float4 v[VL];
 };
 
-// Keys at or past Sk (only in a ragged last tile) load as zeros; they are masked.
-// A full tile (the wave-uniform common case) loads without per-lane tests.
+// Raw buffer descriptor over `bytes` bytes at `base`: loads past the end return zero.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const float* base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base), 0, (int)bytes, 0x00020000);
+}
+__device__ __forceinline__ float4 load16(__amdgpu_buffer_rsrc_t r, uint32_t off) {
+    typedef float f32x4v __attribute__((ext_vector_type(4)));
+    const f32x4v v = __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0);
+    return make_float4(v[0], v[1], v[2], v[3]);
+}
+
+// The tile of keys base .. base + 31, through descriptors that cover just the
+// tile's keys below Sk: keys at or past Sk (a ragged last tile) load as zeros by
+// the range check, with no per-lane test, and their scores are masked. One load
+// path keeps the prefetched registers in place across the loop (two paths
+// merged at the loop head made the compiler copy them, and wait for the loads
+// to land, right after issuing them).
 template <int R, int DV>
 __device__ __forceinline__ void load_tile(WaveRegs<R, DV>& t, const float* kg, const float* vg, int base, int Sk,
                                           int lane) {
     using W = WaveRegs<R, DV>;
-    constexpr int CPR = R / 4;
-    if (base + W::BN <= Sk) {
-#pragma unroll
-        for (int i = 0; i < W::KL; ++i) {
-            const int c = lane + 64 * i;
-            t.k[i] = *(const float4*)(kg + (size_t)(base + c / CPR) * R + (c % CPR) * 4);
-        }
-#pragma unroll
-        for (int i = 0; i < W::VL; ++i) {
-            const int qd = lane + 64 * i;
-            const int kq = qd % (W::BN / 4), dc = qd / (W::BN / 4);
-#pragma unroll
-            for (int j = 0; j < 4; ++j) t.v[i][j] = *(const float4*)(vg + (size_t)(base + 4 * kq + j) * DV + dc * 4);
-        }
-        return;
-    }
+    constexpr int KC = R / 4, VC = DV / 4;  // 16-byte chunks per K row and per V row
+    const uint32_t rows = (uint32_t)(Sk - base < W::BN ? Sk - base : W::BN);
+    const auto kr = tile_rsrc(kg + (size_t)base * R, rows * R * 4);
+    const auto vr = tile_rsrc(vg + (size_t)base * DV, rows * DV * 4);
 #pragma unroll
     for (int i = 0; i < W::KL; ++i) {
         const int c = lane + 64 * i;
-        const int row = c / CPR, part = c % CPR;
-        t.k[i] = base + row < Sk ? *(const float4*)(kg + (size_t)(base + row) * R + part * 4)
-                                 : make_float4(0, 0, 0, 0);
+        t.k[i] = load16(kr, (uint32_t)(((c / KC) * R + (c % KC) * 4) * 4));
     }
 #pragma unroll
     for (int i = 0; i < W::VL; ++i) {
-        const int qd = lane + 64 * i;
-        const int kq = qd % (W::BN / 4), dc = qd / (W::BN / 4);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int key = base + 4 * kq + j;
-            t.v[i][j] = key < Sk ? *(const float4*)(vg + (size_t)key * DV + dc * 4) : make_float4(0, 0, 0, 0);
-        }
+        const int c = lane + 64 * i;
+        t.v[i] = load16(vr, (uint32_t)(((c / VC) * DV + (c % VC) * 4) * 4));
     }
 }
 
@@ -112,23 +115,16 @@ template <int R, int DV>
 __device__ __forceinline__ void store_tile(const WaveRegs<R, DV>& t, WaveTile<R, DV>& tile, int lane) {
     using W = WaveRegs<R, DV>;
     using T = WaveTile<R, DV>;
-    constexpr int CPR = R / 4;
+    constexpr int KC = R / 4, VC = DV / 4;
 #pragma unroll
     for (int i = 0; i < W::KL; ++i) {
         const int c = lane + 64 * i;
-        const int row = c / CPR, part = c % CPR;
-        *(float4*)(tile.k + row * T::KS + part * 4) = t.k[i];
+        *(float4*)(tile.k + (c / KC) * T::KS + (c % KC) * 4) = t.k[i];
     }
 #pragma unroll
     for (int i = 0; i < W::VL; ++i) {
-        const int qd = lane + 64 * i;
-        const int kq = qd % (W::BN / 4), dc = qd / (W::BN / 4);
-        const float4* x = t.v[i];
-        // 4 keys x 4 columns -> 4 rows of V^T, 4 consecutive keys each
-        *(float4*)(tile.vt + (dc * 4 + 0) * T::VS + 4 * kq) = make_float4(x[0].x, x[1].x, x[2].x, x[3].x);
-        *(float4*)(tile.vt + (dc * 4 + 1) * T::VS + 4 * kq) = make_float4(x[0].y, x[1].y, x[2].y, x[3].y);
-        *(float4*)(tile.vt + (dc * 4 + 2) * T::VS + 4 * kq) = make_float4(x[0].z, x[1].z, x[2].z, x[3].z);
-        *(float4*)(tile.vt + (dc * 4 + 3) * T::VS + 4 * kq) = make_float4(x[0].w, x[1].w, x[2].w, x[3].w);
+        const int c = lane + 64 * i;
+        *(float4*)(tile.v + (c / VC) * T::VS + (c % VC) * 4) = t.v[i];
     }
 }
 
@@ -158,16 +154,19 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillP
     __shared__ Smem<R, DV> sm;
 
     const int tid = threadIdx.x;
-    const int lane = tid & 63, wave = tid >> 6;
+    const int lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int grp = lane >> 4, n = lane & 15;  // lane group, and the query (B column) the lane serves
 
     // workgroup -> (query block, head, sequence): ranked by causal prefix length,
     // longest first, with the heads and sequences of one rank adjacent, so that the
     // round-robin dispatch over the XCDs deals every XCD the same mix of long and
-    // short blocks
+    // short blocks; odd rounds of 256 workgroups take their positions in reverse
     const int nqb = (p.Sq + kRows - 1) / kRows;
-    const int rank = (int)(blockIdx.x / ((unsigned)p.Hq * p.B));
-    const int hb = (int)(blockIdx.x % ((unsigned)p.Hq * p.B));
+    const unsigned round = blockIdx.x / 256u, first = round * 256u;
+    const unsigned in_round = (gridDim.x - first < 256u ? gridDim.x - first : 256u);
+    const unsigned pos = (round & 1u) ? first + in_round - 1u - (blockIdx.x - first) : blockIdx.x;
+    const int rank = (int)(pos / ((unsigned)p.Hq * p.B));
+    const int hb = (int)(pos % ((unsigned)p.Hq * p.B));
     const int qb = p.causal ? nqb - 1 - rank : rank;
     const int h = hb % p.Hq;
     const int g = h / p.G;
@@ -275,11 +274,11 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillP
         for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
             for (int d = 0; d < DBLK; ++d) {
-                const float4 a = *(const float4*)(tile.vt + (d * 16 + n) * VS + kb * 16 + 4 * grp);
-                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, s[kb][0], o[d], 0, 0, 0);
-                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, s[kb][1], o[d], 0, 0, 0);
-                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, s[kb][2], o[d], 0, 0, 0);
-                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.w, s[kb][3], o[d], 0, 0, 0);
+                const float* vp = tile.v + (kb * 16 + 4 * grp) * VS + d * 16 + n;
+                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(vp[0], s[kb][0], o[d], 0, 0, 0);
+                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(vp[VS], s[kb][1], o[d], 0, 0, 0);
+                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(vp[2 * VS], s[kb][2], o[d], 0, 0, 0);
+                o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(vp[3 * VS], s[kb][3], o[d], 0, 0, 0);
             }
         wave_lds_sync();  // the tile's operand reads are done before the next store
     }
