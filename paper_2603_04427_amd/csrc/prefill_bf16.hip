@@ -69,31 +69,35 @@ struct Smem {
 
 // Global->LDS copies of one 64-key K and V tile (global_load_lds, 16 bytes per
 // lane, each wave filling 1 KB of consecutive LDS). Which 16-byte chunk of which
-// row a lane copies does not depend on the tile, so its element offset inside
-// a tile is computed once (TileLanes); a tile then only adds its first row.
+// row a lane copies does not depend on the tile, so its byte offset inside a
+// tile is computed once (TileLanes); a tile then only adds its first row. Copy
+// i of a lane takes the chunk NT i further, i.e. NT / (W / 8) rows further down
+// at the same chunk position: the row swizzles repeat with a period that
+// divides that step, so copy i's offset is copy 0's plus a constant, which the
+// wave-uniform global base absorbs. One offset register per tile is kept.
 template <int R, int DV, int NT>
 struct TileLanes {
     static constexpr int KC = kBN * R / 8;   // 16-byte chunks in the K tile
     static constexpr int VC = kBN * DV / 8;  // ... and in the V tile
     static constexpr int KL = (KC + NT - 1) / NT;
     static constexpr int VL = (VC + NT - 1) / NT;
-    uint32_t k_off[KL];  // byte offset (in the tile) of each K chunk this lane copies
-    uint32_t v_off[VL];
+    static constexpr int KSTEP = NT / (R / 8);   // rows between a lane's copies i and i + 1
+    static constexpr int VSTEP = NT / (DV / 8);
+    // swizzle periods in rows: swz<W, false> repeats every RPL * CPR rows,
+    // swz<W, true> every RPL * CPR / 4
+    static constexpr int KPER = ((256 / (2 * R)) > 0 ? 256 / (2 * R) : 1) * (R / 8);
+    static constexpr int VPER = ((256 / (2 * DV)) > 0 ? 256 / (2 * DV) : 1) * (DV / 8) / 4;
+    static_assert(KL == 1 || KSTEP % KPER == 0, "K copy offsets are not a constant stride apart");
+    static_assert(VL == 1 || VSTEP % VPER == 0, "V copy offsets are not a constant stride apart");
+    uint32_t k_off;  // byte offset (in the tile) of this lane's first K chunk
+    uint32_t v_off;
     int tid_;
 
     __device__ __forceinline__ explicit TileLanes(int tid) : tid_(tid) {
-#pragma unroll
-        for (int i = 0; i < KL; ++i) {
-            const int ci = tid + i * NT;
-            const int r = ci / (R / 8), pos = ci % (R / 8);
-            k_off[i] = (uint32_t)((r * R + (pos ^ swz<R, false>(r)) * 8) * 2);
-        }
-#pragma unroll
-        for (int i = 0; i < VL; ++i) {
-            const int ci = tid + i * NT;
-            const int r = ci / (DV / 8), pos = ci % (DV / 8);
-            v_off[i] = (uint32_t)((r * DV + (pos ^ swz<DV, true>(r)) * 8) * 2);
-        }
+        const int kr = tid / (R / 8), kp = tid % (R / 8);
+        k_off = (uint32_t)((kr * R + (kp ^ swz<R, false>(kr)) * 8) * 2);
+        const int vr = tid / (DV / 8), vp = tid % (DV / 8);
+        v_off = (uint32_t)((vr * DV + (vp ^ swz<DV, true>(vr)) * 8) * 2);
     }
     // tile rows of the chunks, recomputed (needed only for a ragged last tile)
     __device__ __forceinline__ int k_row(int i) const { return (tid_ + i * NT) / (R / 8); }
@@ -102,7 +106,7 @@ struct TileLanes {
 
 // Issue the copies of the tile starting at key `base` (wave `wave` copies its
 // 1 KB slices). A full tile needs no vector arithmetic: the global base and the
-// LDS destination are wave-uniform and the lane offsets are precomputed. Rows
+// LDS destination are wave-uniform and the lane offset is precomputed. Rows
 // at or past Sk (only in a ragged last tile) re-read row Sk - 1: finite values,
 // masked later.
 template <int R, int DV, int NT>
@@ -116,28 +120,34 @@ __device__ __forceinline__ void load_tile(const TileLanes<R, DV, NT>& tl, uint16
 #pragma unroll
         for (int i = 0; i < T::KL; ++i) {
             if (T::KC % NT != 0 && wave_base + i * NT >= T::KC) break;
-            copy16_to_lds(kt, tl.k_off[i], ks + (wave_base + i * NT) * 8);
+            copy16_to_lds(kt + i * T::KSTEP * R * 2, tl.k_off, ks + (wave_base + i * NT) * 8);
         }
 #pragma unroll
         for (int i = 0; i < T::VL; ++i) {
             if (T::VC % NT != 0 && wave_base + i * NT >= T::VC) break;
-            copy16_to_lds(vt, tl.v_off[i], vs + (wave_base + i * NT) * 8);
+            copy16_to_lds(vt + i * T::VSTEP * DV * 2, tl.v_off, vs + (wave_base + i * NT) * 8);
         }
         return;
     }
+    // A ragged tile clamps rows past the end to row `last` by lowering the
+    // offset. The copy's vector offset is unsigned, so here every copy keeps the
+    // tile's own base and adds its stride to the offset: the clamped offset then
+    // stays non-negative even where `last` lies above copy i's first row.
     const int last = Sk - base - 1;
 #pragma unroll
     for (int i = 0; i < T::KL; ++i) {
         if (T::KC % NT != 0 && wave_base + i * NT >= T::KC) break;
         const int kr = tl.k_row(i);
-        const uint32_t off = kr > last ? tl.k_off[i] - (kr - last) * R * 2 : tl.k_off[i];
+        const uint32_t oi = tl.k_off + (uint32_t)(i * T::KSTEP * R * 2);
+        const uint32_t off = kr > last ? oi - (uint32_t)((kr - last) * R * 2) : oi;
         copy16_to_lds(kt, off, ks + (wave_base + i * NT) * 8);
     }
 #pragma unroll
     for (int i = 0; i < T::VL; ++i) {
         if (T::VC % NT != 0 && wave_base + i * NT >= T::VC) break;
         const int vr = tl.v_row(i);
-        const uint32_t off = vr > last ? tl.v_off[i] - (vr - last) * DV * 2 : tl.v_off[i];
+        const uint32_t oi = tl.v_off + (uint32_t)(i * T::VSTEP * DV * 2);
+        const uint32_t off = vr > last ? oi - (uint32_t)((vr - last) * DV * 2) : oi;
         copy16_to_lds(vt, off, vs + (wave_base + i * NT) * 8);
     }
 }
