@@ -128,7 +128,6 @@ tk_status decode_impl(const void* Q, const void* K_cache, const void* V_cache, v
     p.mb = paged ? max_blocks_per_seq : 0;
     p.num_blocks = paged ? num_blocks : 0;
     p.n_split = pl.n_split;
-    p.split_len = pl.split_len;
     p.qscale = resolve_scale(scale, r) * tk::kLog2e;
     return tk::launch_decode(p, r, d_v, hg, key_format(k_dtype), paged, stream);
 }

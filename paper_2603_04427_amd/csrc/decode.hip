@@ -7,9 +7,13 @@
 //
 //  * Grouped-query packing: a workgroup serves all HG query heads that share a
 //    KV head, so each K/V byte crosses HBM once for HG heads.
-//  * Each wave streams 64-token chunks with 16-byte loads per lane, all of a
-//    chunk's K and V loads issued before any arithmetic: key rows tile the lanes
-//    (LPT lanes per row, one 16-byte slice each), value rows likewise.
+//  * Each wave streams 32- or 64-token chunks with 16-byte loads per lane, all
+//    of a chunk's K and V loads issued before any arithmetic: key rows tile the
+//    lanes (LPT lanes per row, one 16-byte slice each), value rows likewise.
+//    The waves of a workgroup take consecutive chunks (one round), and the
+//    splits of a (sequence, head group) take the rounds in turn, so together
+//    they read one contiguous stream of each cache rather than n_split
+//    separate ones.
 //  * Scores: per-lane partial dot products over the lane's slice of r, reduced
 //    across the LPT lanes of a row with DPP. The softmax scale and log2(e) are
 //    folded into the fp32 query once, so the softmax uses exp2 directly; for
@@ -374,7 +378,6 @@ __global__ __launch_bounds__(kDecodeThreads, (decode_min_blocks<HG, KF>())) void
     const int g = blockIdx.y / groups_per_kv;
     const int h0 = g * p.G + (blockIdx.y % groups_per_kv) * HG;
     const int b = blockIdx.z;
-    const int split_begin = split * p.split_len;
 
     // this lane's query slice as packed bf16 pairs (exact; the scale is applied in fp32)
     uint32_t qp[HG][S::QW];
@@ -415,17 +418,17 @@ __global__ __launch_bounds__(kDecodeThreads, (decode_min_blocks<HG, KF>())) void
     bool bad_block = false;
     uint16_t* p16 = (uint16_t*)p_lds[wave];
 
-    // Chunks ts, ts + kStride, ... of this wave; with PIPE the next chunk's loads
-    // are issued before the current one is processed. For a contiguous cache the
-    // first chunk is requested before the context length is read (rows up to
-    // max_ctx are readable), so the length's round trip overlaps the stream;
-    // paged caches wait for it, because table entries past the context need not
-    // be valid.
+    // Chunks ts, ts + kStride, ... of this wave: a round is kDecodeWaves chunks,
+    // one per wave, and split s takes rounds s, s + n_split, ... With PIPE the
+    // next chunk's loads are issued before the current one is processed. For a
+    // contiguous cache the first chunk is requested before the context length
+    // is read (rows up to max_ctx are readable), so the length's round trip
+    // overlaps the stream; paged caches wait for it, because table entries past
+    // the context need not be valid.
     using C = Chunk<R, DV, HG, KF, CH>;
-    constexpr int kStride = kDecodeWaves * CH;
-    int ts = split_begin + wave * CH;
-    int first_avail = split_begin + p.split_len;
-    first_avail = first_avail < p.max_ctx ? first_avail : p.max_ctx;
+    const int kStride = p.n_split * kDecodeWaves * CH;
+    int ts = (split * kDecodeWaves + wave) * CH;
+    int first_avail = p.max_ctx;
     C ca;
     bool ok_a = true;
     if constexpr (!PAGED) {
@@ -434,8 +437,7 @@ __global__ __launch_bounds__(kDecodeThreads, (decode_min_blocks<HG, KF>())) void
     }
     int L = load_uniform(p.ctx_lens + b);
     L = L < 0 ? 0 : (L > p.max_ctx ? p.max_ctx : L);
-    int split_end = split_begin + p.split_len;
-    split_end = split_end < L ? split_end : L;
+    const int split_end = L;  // every split walks to the end of the context
     if constexpr (PAGED) {
         first_avail = split_end;
         if (ts < first_avail) ok_a = load_chunk<R, DV, HG, KF, CH, PAGED>(ca, p, b, g, ts, first_avail, lane);

@@ -30,14 +30,14 @@ struct DecodeParams {
     uint16_t* o;                // [B, Hq, DV] bf16
     int B, Hq, Hkv, G, max_ctx;
     int bs_log2, mb, num_blocks;
-    int n_split, split_len;     // split_len: tokens per split, a multiple of 256
+    int n_split;                // splits of each (sequence, head group): split s takes rounds s, s + n_split, ...
     float qscale;               // softmax scale * log2(e)
 };
 
 struct DecodePlan {
     int heads_per_group;  // query heads one workgroup serves (divides G, <= 8)
     int n_split;
-    int split_len;
+    int split_len;  // tokens per split, a multiple of 256 (planning: n_split = ceil(max_ctx / split_len))
     size_t counter_bytes;  // leading counter region of the workspace (256-byte multiple)
     size_t ws_bytes;
 };
