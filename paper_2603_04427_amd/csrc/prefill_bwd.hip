@@ -16,7 +16,10 @@
 //    read and dS^T straight from the accumulators. It also writes D, computed
 //    from the lane's own dO and O slices.
 //  * bwd_dkdv_kernel, key-major: a wave owns 32 keys (K and V rows in
-//    registers) and walks the query tiles of every head of the group. Scores are
+//    registers) and walks the query tiles of every head of the group, from the
+//    last tile down to its diagonal with the heads innermost, so that all key
+//    blocks of a KV sequence read the same Q and dO tile at about the same
+//    time (one fetch into the XCD's L2 serves them all). Scores are
 //    S = Q K^T, so a lane owns one key and P and dS leave the accumulators
 //    already in the A-operand layout of dV = P^T dO and dK = dS^T Q, whose B
 //    operands (dO and Q with 8 query rows per lane) come from the transposing
@@ -353,15 +356,15 @@ struct alignas(16) KvSmem {
     float dl[2][kT];    // D of the tile's rows
 };
 
-// Issue the copies of query tile `it` (head g G + it / n_rt, rows from
-// (t0 + it % n_rt) 64) into buffer `buf`: Q and dO rows by all waves, the rows'
+// Issue the copies of query tile `it` (head g G + it % G, rows from
+// (t0 + n_rt - 1 - it / G) 64) into buffer `buf`: Q and dO rows by all waves, the rows'
 // lse2 by wave 0 and D by wave 1 (one float per lane, rows clamped to Sq - 1).
 template <int R, int DV>
 __device__ __forceinline__ void issue_qtile(const PrefillBwdParams& p, KvSmem<R, DV>& sm, const TileCopy<R>& qc,
                                             const TileCopy<DV>& dc, int it, int buf, int b, int g, int t0,
                                             int n_rt, int wave, int lane) {
-    const int hh = g * p.G + it / n_rt;
-    const int row0 = (t0 + it % n_rt) * kT;
+    const int hh = g * p.G + it % p.G;
+    const int row0 = (t0 + n_rt - 1 - it / p.G) * kT;
     const size_t rowq = (size_t)b * p.Hq + hh;
     qc.issue((const uint16_t*)p.q + rowq * p.Sq * R, row0, p.Sq, sm.q[buf], wave);
     dc.issue((const uint16_t*)p.dout + rowq * p.Sq * DV, row0, p.Sq, sm.d[buf], wave);
@@ -411,7 +414,7 @@ __global__ __launch_bounds__(kThreads, R + DV >= 192 ? 1 : 2) void bwd_dkdv_kern
     const int t0 = first_row / kT;
     const int nt = (p.Sq + kT - 1) / kT;
     const int n_rt = nt - t0;
-    const int n_iter = n_rt * p.G;  // (head, tile) pairs
+    const int n_iter = n_rt * p.G;  // (tile, head) pairs, tiles descending, heads innermost
 
     const TileCopy<R> qc(wave, lane);
     const TileCopy<DV> dc(wave, lane);
@@ -447,7 +450,7 @@ __global__ __launch_bounds__(kThreads, R + DV >= 192 ? 1 : 2) void bwd_dkdv_kern
 
     for (int it = 0; it < n_iter; ++it) {
         const int cur = it & 1;
-        const int i0 = (t0 + it % n_rt) * kT;  // first query row of the tile
+        const int i0 = (t0 + n_rt - 1 - it / p.G) * kT;  // first query row of the tile
         if (it + 1 < n_iter) issue_qtile<R, DV>(p, sm, qc, dc, it + 1, cur ^ 1, b, g, t0, n_rt, wave, lane);
         if (!(p.causal && i0 + kT - 1 + off < k0)) {  // some row of the tile sees the wave's keys
             const uint16_t* qs = sm.q[cur];
