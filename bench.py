@@ -43,6 +43,9 @@ The JSON line reports, besides the contract fields:
                 standard-width bf16 keys (r = 128, same values), and the thin-key
                 speedup over them next to the byte (decode) or FLOP (prefill)
                 ratio that bounds it.
+Every line but the headline times at least 50 ms of calls (more calls for the
+short kernels, after a quarter as many extra warm-up calls) and reports the
+number it timed in `timed_calls`; the headline times exactly --steps calls.
 """
 from __future__ import annotations
 
@@ -58,6 +61,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "thin-key decode-attn HBM GB/s (% peak); prefill-attn TFLOP/s (% MFMA peak)"
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pmc_traffic.json")
+SECONDARY_MIN_S = 0.05  # seconds of timed calls at least, for every line but the headline
 KERNEL_SOURCES = {"decode": "paper_2603_04427_amd/csrc/decode.hip",
                   "prefill_bf16": "paper_2603_04427_amd/csrc/prefill_bf16.hip",
                   "prefill_f32": "paper_2603_04427_amd/csrc/prefill_f32.hip",
@@ -71,7 +75,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=200, help="timed steps")
     ap.add_argument("--warmup", type=int, default=500,
                     help="untimed warm-up steps (enough for the GPU to reach its steady clocks; the "
-                         "secondary workloads take a tenth of it, prefill at most 3)")
+                         "secondary workloads take a tenth of it, prefill at most 3, then the warm-up "
+                         "that their 50 ms minimum of timed calls adds)")
     ap.add_argument("--rotate", type=int, default=8, help="cache copies cycled through in the timed loop")
     ap.add_argument("--only", default=None, help="time just this workload (e.g. for profiling)")
     ap.add_argument("--no-secondary", action="store_true")
@@ -101,16 +106,32 @@ def traffic_for(workload: str, kind: str):
     return rec.get("bytes_per_call")
 
 
-def time_calls(calls, steps: int, warmup: int):
+def time_calls(calls, steps: int, warmup: int, min_timed_s: float = 0.0):
     """Warm up, then time ``steps`` calls (cycling through ``calls``).
 
-    Returns (wall seconds per step, event seconds per step). The wall clock is
-    bracketed by device synchronisation; the events sit on the launch stream."""
+    With ``min_timed_s`` > 0 (the secondary workloads; the headline line times
+    exactly the steps it is given) the timed calls are raised, up to 5000, until
+    they cover at least that many seconds, and as many extra warm-up calls as a
+    quarter of them run first: a few calls of a kernel of some microseconds would
+    otherwise time the host's launch gaps and the clock's ramp, not the kernel.
+
+    Returns (wall seconds per step, event seconds per step, timed calls). The
+    wall clock is bracketed by device synchronisation; the events sit on the
+    launch stream."""
     import torch
     n = len(calls)
     for i in range(warmup):
         calls[i % n]()
     torch.cuda.synchronize()
+    if min_timed_s > 0:
+        t = time.perf_counter()
+        calls[0]()
+        torch.cuda.synchronize()
+        one = max(time.perf_counter() - t, 1e-6)
+        steps = max(steps, min(5000, int(min_timed_s / one) + 1))
+        for i in range(steps // 4):
+            calls[i % n]()
+        torch.cuda.synchronize()
     st = torch.cuda.current_stream()
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
@@ -121,7 +142,7 @@ def time_calls(calls, steps: int, warmup: int):
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
     ev = e0.elapsed_time(e1) / 1e3 / steps
-    return wall, ev
+    return wall, ev, steps
 
 
 def decode_setup(spec, dev, rotate: int):
@@ -144,23 +165,23 @@ def decode_setup(spec, dev, rotate: int):
     return calls
 
 
-def decode_result(name, spec, calls, steps, warmup):
+def decode_result(name, spec, calls, steps, warmup, min_timed_s=0.0):
     from paper_2603_04427_amd import accounting as acc
-    wall, ev = time_calls(calls, steps, warmup)
+    wall, ev, steps = time_calls(calls, steps, warmup, min_timed_s)
     nbytes = acc.decode_bytes(spec.lens, spec.h_q, spec.h_kv, spec.r, spec.d_v, spec.k_dtype,
                               spec.blocks_per_seq if spec.paged else None)
     achieved = nbytes / ev / 1e9
     traffic = traffic_for(name, "decode")
     return {
         "workload": name, "value": round(nbytes / wall / 1e9, 1), "unit": "GB/s",
-        "ms_per_call": round(wall * 1e3, 5),
+        "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": acc.HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / acc.HBM_PEAK_GBS, 4), "traffic": traffic,
                      "algorithmic_bytes": nbytes, "kernel_ms": round(ev * 1e3, 5)},
     }
 
 
-def prefill_result(name, spec, dev, steps, warmup):
+def prefill_result(name, spec, dev, steps, warmup, min_timed_s=0.0):
     import torch
     from paper_2603_04427_amd import accounting as acc
     from paper_2603_04427_amd import prepare_prefill
@@ -168,7 +189,7 @@ def prefill_result(name, spec, dev, steps, warmup):
 
     p = make_prefill(spec, device=dev)
     call = prepare_prefill(p["q"], p["k"], p["v"], causal=spec.causal, scale=spec.softmax_scale)
-    wall, ev = time_calls([call], steps, warmup)
+    wall, ev, steps = time_calls([call], steps, warmup, min_timed_s)
     flops = acc.prefill_flops(spec.batch, spec.h_q, spec.seq_q, spec.seq_k, spec.r, spec.d_v, spec.causal)
     peak = acc.BF16_MFMA_PEAK_TFLOPS if spec.dtype == "bf16" else acc.FP32_MFMA_PEAK_TFLOPS
     achieved = flops / ev / 1e12
@@ -177,14 +198,14 @@ def prefill_result(name, spec, dev, steps, warmup):
     torch.cuda.empty_cache()
     return {
         "workload": name, "value": round(flops / wall / 1e12, 2), "unit": "TFLOP/s",
-        "ms_per_call": round(wall * 1e3, 5), "dtype": spec.dtype,
+        "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps, "dtype": spec.dtype,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": traffic_for(name, kind),
                      "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5)},
     }
 
 
-def backward_result(name, spec, dev, steps, warmup):
+def backward_result(name, spec, dev, steps, warmup, min_timed_s=0.0):
     """tk_attn_prefill_backward (both kernels) on a prefill shape; the forward with
     log-sum-exp runs once, untimed, to produce O and lse."""
     import torch
@@ -197,7 +218,7 @@ def backward_result(name, spec, dev, steps, warmup):
     o, lse = tk_attn_prefill_lse(p["q"], p["k"], p["v"], causal=spec.causal, scale=spec.softmax_scale)
     call = prepare_prefill_backward(p["q"], p["k"], p["v"], o, do, lse, causal=spec.causal,
                                     scale=spec.softmax_scale)
-    wall, ev = time_calls([call], steps, warmup)
+    wall, ev, steps = time_calls([call], steps, warmup, min_timed_s)
     flops = acc.prefill_backward_flops(spec.batch, spec.h_q, spec.seq_q, spec.seq_k, spec.r, spec.d_v,
                                        spec.causal)
     peak = acc.BF16_MFMA_PEAK_TFLOPS
@@ -206,7 +227,7 @@ def backward_result(name, spec, dev, steps, warmup):
     torch.cuda.empty_cache()
     return {
         "workload": name, "value": round(flops / wall / 1e12, 2), "unit": "TFLOP/s",
-        "ms_per_call": round(wall * 1e3, 5), "dtype": spec.dtype,
+        "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps, "dtype": spec.dtype,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": traffic_for(name, "prefill_bwd"),
                      "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5),
@@ -234,7 +255,7 @@ def batch_sweep(dev, steps, warmup, rotate):
         for tag, r in (("thin", 32), ("full", 128)):
             spec = replace(base, name=f"decode_b{B}_{tag}", batch=B, r=r)
             calls = decode_setup(spec, dev, rotate)
-            res = decode_result(spec.name, spec, calls, steps, warmup)
+            res = decode_result(spec.name, spec, calls, steps, warmup, SECONDARY_MIN_S)
             del calls
             torch.cuda.empty_cache()
             row[tag] = {"kernel_ms": res["roofline"]["kernel_ms"], "GBps": res["roofline"]["achieved"],
@@ -252,7 +273,7 @@ PROJECTION_CASES = {  # (B, S, d_model, h_q, h_kv, r, d_v): a converted layer's 
 }
 
 
-def projection_result(name, B, S, d_model, h_q, h_kv, r, dv, dev, steps, warmup):
+def projection_result(name, B, S, d_model, h_q, h_kv, r, dv, dev, steps, warmup, min_timed_s=0.0):
     """q' = x W_Q', k' = x W_K' and v = x W_V of a layer converted to thin keys:
     three tk_project_heads calls per step, random bf16 weights of the converted shapes."""
     import torch
@@ -271,14 +292,14 @@ def projection_result(name, B, S, d_model, h_q, h_kv, r, dv, dev, steps, warmup)
     def step():
         for c in calls:
             c()
-    wall, ev = time_calls([step], steps, warmup)
+    wall, ev, steps = time_calls([step], steps, warmup, min_timed_s)
     flops = 2 * B * S * d_model * cols
     achieved = flops / ev / 1e12
     del x, calls
     torch.cuda.empty_cache()
     return {
         "workload": name, "value": round(flops / wall / 1e12, 2), "unit": "TFLOP/s",
-        "ms_per_call": round(wall * 1e3, 5), "dtype": "bf16",
+        "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps, "dtype": "bf16",
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": acc.BF16_MFMA_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / acc.BF16_MFMA_PEAK_TFLOPS, 4),
                      "traffic": None, "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5),
@@ -290,7 +311,7 @@ APPEND_CASES = {"cache_append_s8192": (4, 8192, "bf16"), "cache_append_fp8_s8192
                 "cache_append_int4_s8192": (4, 8192, "int4"), "cache_append_decode_b16": (16, 1, "bf16")}
 
 
-def append_result(name, B, Hkv, T, r, dv, kdt, dev, steps, warmup):
+def append_result(name, B, Hkv, T, r, dv, kdt, dev, steps, warmup, min_timed_s=0.0):
     """tk_cache_append of T new tokens per (sequence, KV head) into a contiguous cache
     with bf16, fp8 or 4-bit keys (``kdt``)."""
     import torch
@@ -306,7 +327,7 @@ def append_result(name, B, Hkv, T, r, dv, kdt, dev, steps, warmup):
     ks = torch.zeros(B, Hkv, T, dtype=torch.float32, device=dev) if quant else None
     pos = torch.zeros(B, dtype=torch.int32, device=dev)
     call = prepare_cache_append(kn, vn, pos, kc, vc, k_scale=ks)
-    wall, ev = time_calls([call], steps, warmup)
+    wall, ev, steps = time_calls([call], steps, warmup, min_timed_s)
     tokens = B * Hkv * T
     key_out = {"bf16": r * 2, "fp8": r + 4, "int4": r // 2 + 4}[kdt]
     nbytes = tokens * (r * 2 + dv * 2) + B * 4 + tokens * key_out + tokens * dv * 2
@@ -315,7 +336,7 @@ def append_result(name, B, Hkv, T, r, dv, kdt, dev, steps, warmup):
     from paper_2603_04427_amd import accounting as acc
     return {
         "workload": name, "value": round(nbytes / wall / 1e9, 1), "unit": "GB/s",
-        "ms_per_call": round(wall * 1e3, 5),
+        "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps,
         "roofline": {"bound": "hbm", "achieved": round(nbytes / ev / 1e9, 1), "peak": acc.HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(nbytes / ev / 1e9 / acc.HBM_PEAK_GBS, 4),
                      "traffic": traffic_for(name, "append"), "algorithmic_bytes": nbytes,
@@ -514,13 +535,14 @@ def main():
             big = spec.batch * spec.h_kv * spec.ctx * (spec.r + spec.d_v) * 2 > (1 << 30)
             calls = decode_setup(spec, dev, 1 if big else args.rotate)
             steps = args.steps if main else max(10, args.steps // 10)
-            res = decode_result(name, spec, calls, steps, args.warmup if main else max(10, args.warmup // 10))
+            res = decode_result(name, spec, calls, steps, args.warmup if main else max(10, args.warmup // 10),
+                                0.0 if main else SECONDARY_MIN_S)
             res["rotate"] = len(calls)
             del calls
             torch.cuda.empty_cache()
         else:
             steps = args.steps if main else max(5, args.steps // 20)
-            res = prefill_result(name, spec, dev, steps, min(args.warmup, 3))
+            res = prefill_result(name, spec, dev, steps, min(args.warmup, 3), 0.0 if main else SECONDARY_MIN_S)
         return res
 
     for name in order:
@@ -545,7 +567,7 @@ def main():
         for base in ("mistral_prefill_s8192", "mistral_prefill_s8192_fullkey"):
             print(f"bench: timing {base}_backward", file=sys.stderr, flush=True)
             backward.append(backward_result(base + "_backward", workloads[base], dev, max(5, args.steps // 20),
-                                            min(args.warmup, 3)))
+                                            min(args.warmup, 3), SECONDARY_MIN_S))
         if len(backward) == 2:
             thin, full = backward
             full["thin_key_speedup"] = round(full["roofline"]["kernel_ms"] / thin["roofline"]["kernel_ms"], 3)
@@ -556,12 +578,13 @@ def main():
         for name, (B, T, kdt) in APPEND_CASES.items():
             print(f"bench: timing {name}", file=sys.stderr, flush=True)
             appends.append(append_result(name, B, 8, T, 32, 128, kdt, dev, max(10, args.steps // 10),
-                                         args.warmup))
+                                         args.warmup, SECONDARY_MIN_S))
     projections = []
     if not (args.only or args.no_secondary):
         for name, shape in PROJECTION_CASES.items():
             print(f"bench: timing {name}", file=sys.stderr, flush=True)
-            projections.append(projection_result(name, *shape, dev, max(10, args.steps // 10), min(args.warmup, 5)))
+            projections.append(projection_result(name, *shape, dev, max(10, args.steps // 10), min(args.warmup, 5),
+                                                 SECONDARY_MIN_S))
     sweep = []
     if not (args.only or args.no_secondary or args.no_fullkey):
         print("bench: timing the decode batch sweep", file=sys.stderr, flush=True)
