@@ -14,12 +14,17 @@
 //    splits of a (sequence, head group) take the rounds in turn, so together
 //    they read one contiguous stream of each cache rather than n_split
 //    separate ones.
-//  * Scores: per-lane partial dot products over the lane's slice of r, reduced
-//    across the LPT lanes of a row with DPP. The softmax scale and log2(e) are
-//    folded into the fp32 query once, so the softmax uses exp2 directly; for
-//    fp8 keys the per-(token, head) scale multiplies the reduced dot product.
-//  * Online softmax per head with a wave-wide running maximum; probabilities go
-//    through a small per-wave LDS table to the lanes that own the value columns.
+//  * Scores: per-lane partial dot products over the lane's slice of r (the
+//    query kept as exact bf16 pairs), reduced across the LPT lanes of a row
+//    with DPP. One fp32 multiply by the softmax scale times log2(e) (and, for
+//    quantised keys, the token's key scale) turns the reduced dot product into
+//    a log2-domain logit, so the softmax uses exp2 directly.
+//  * Online softmax per head: each score is exponentiated once, by the lane
+//    that owns its head, against a lazy reference maximum that moves only when
+//    a score exceeds it by more than 8 in log2 units, a factor of 256 (a wave
+//    ballot, then a cross-lane reduction, almost never after a stream's first
+//    chunk); probabilities go through a small per-wave LDS table to the lanes
+//    that own the value columns.
 //  * The waves of a workgroup merge their (max, sum, output) triples in LDS
 //    and write one partial per (sequence, head, split). The last workgroup of a
 //    (sequence, head group) to finish - found with an agent-scope counter in the

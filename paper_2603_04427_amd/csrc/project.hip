@@ -42,11 +42,13 @@ struct ProjTile {
     uint16_t x[kStages][BM * kPBK];  // token rows of the tile (same swizzle)
 };
 
-// Chunk kc (0..3) of tile row r sits in slot 4 r + (kc ^ ((r / 2) % 4)). Rows are
-// 64 bytes, so two rows share one 128-byte bank period; the rotation makes the
-// same chunk of any 8 consecutive rows cover all 32 banks. The map is its own
-// inverse: slot 4 r + q holds chunk q ^ ((r / 2) % 4).
-__device__ __forceinline__ int sw(int r, int kc) { return r * kPBK + ((kc ^ ((r >> 1) & 3)) << 3); }
+// Chunk kc (0..3) of tile row r sits in slot 4 r + (kc ^ ((r / 4) % 4)). Rows are
+// 64 bytes, so four rows share one 256-byte line of the 64 LDS banks; the
+// rotation gives the same chunk of the rows r, r + 4, r + 8, r + 12 four
+// different 16-byte bank groups, so the 16 consecutive rows one quarter-wave
+// reads cover all 64 banks once. The map is its own inverse: slot 4 r + q
+// holds chunk q ^ ((r / 4) % 4).
+__device__ __forceinline__ int sw(int r, int kc) { return r * kPBK + ((kc ^ ((r >> 2) & 3)) << 3); }
 
 template <int N>
 __device__ __forceinline__ void wait_copies(bool next_in_flight) {
@@ -83,19 +85,19 @@ __global__ __launch_bounds__(proj_threads<BN>(), 1) void project_kernel(const Pr
     const int col = lane & 31, half = lane >> 5;
 
     // Copy i of this lane fills LDS slot i * 256 + tid of the tile: row slot / 4,
-    // chunk (slot % 4) ^ ((row / 2) % 4) of that row in the matrix. Rows past the
+    // chunk (slot % 4) ^ ((row / 4) % 4) of that row in the matrix. Rows past the
     // matrix re-read its last row (finite values whose outputs are not stored).
     const int wlast = (p.N - n_base < kPBN ? p.N - n_base : kPBN) - 1;
     const int xlast = (p.M - m_base < kPBM ? p.M - m_base : kPBM) - 1;
     uint32_t woff[kWCopies], xoff[kXCopies];
 #pragma unroll
     for (int i = 0; i < kWCopies; ++i) {
-        const int slot = i * kPThreads + tid, r = slot >> 2, kc = (slot & 3) ^ ((r >> 1) & 3);
+        const int slot = i * kPThreads + tid, r = slot >> 2, kc = (slot & 3) ^ ((r >> 2) & 3);
         woff[i] = (uint32_t)(((r < wlast ? r : wlast) * p.K + kc * 8) * 2);
     }
 #pragma unroll
     for (int i = 0; i < kXCopies; ++i) {
-        const int slot = i * kPThreads + tid, r = slot >> 2, kc = (slot & 3) ^ ((r >> 1) & 3);
+        const int slot = i * kPThreads + tid, r = slot >> 2, kc = (slot & 3) ^ ((r >> 2) & 3);
         xoff[i] = (uint32_t)(((r < xlast ? r : xlast) * p.K + kc * 8) * 2);
     }
     const char* wg = (const char*)((const uint16_t*)p.wt + (size_t)n_base * p.K);
