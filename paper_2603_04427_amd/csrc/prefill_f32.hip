@@ -47,7 +47,7 @@ constexpr int kRows = 16;  // query rows per workgroup
 
 // Keys per tile: 32 (two 16-key blocks). A wave's tile then costs 32 (R + DV) / 64
 // floats of prefetch registers per lane, and at the GPT-2 shape (r 16, d_v 64)
-// the workgroup's four tiles take 44 KB of LDS, so three workgroups share a CU
+// the workgroup's four tiles take 42 KB of LDS, so three workgroups share a CU
 // and each SIMD interleaves three waves: while one waits on its dependent
 // score -> softmax -> value chain, another issues matrix products (with 64-key
 // tiles only one workgroup fits and that chain leaves the matrix core idle for
@@ -56,7 +56,7 @@ template <int R, int DV>
 struct alignas(16) WaveTile {
     static constexpr int BN = 32;
     static constexpr int KB = BN / 32;  // 32-key blocks per tile
-    static constexpr int KS = R + 4;    // floats per K row in LDS (16-byte pad)
+    static constexpr int KS = R;        // floats per K row in LDS (16-byte chunks swizzled by kpos)
     static constexpr int VS = DV + 4;   // floats per V row in LDS (16-byte pad)
     float k[BN * KS];
     float v[BN * VS];
@@ -111,6 +111,18 @@ __device__ __forceinline__ void load_tile(WaveRegs<R, DV>& t, const float* kg, c
     }
 }
 
+// Position of 16-byte chunk c of K row r in LDS: rows are R floats, so 256 / (4 R)
+// of them share one 256-byte line of the 64 banks (at least one); rotating the
+// chunk by the row's line index makes the 16 rows a quarter-wave reads at one
+// chunk fall on 16 different 16-byte bank groups, and the stores of whole rows
+// stay contiguous per line.
+template <int R>
+__device__ __forceinline__ int kpos(int r, int c) {
+    constexpr int RPL = (64 / R) > 0 ? 64 / R : 1;  // rows per 256-byte line
+    constexpr int M = (R / 4 < 16 ? R / 4 : 16) - 1;
+    return c ^ ((r / RPL) & M);
+}
+
 template <int R, int DV>
 __device__ __forceinline__ void store_tile(const WaveRegs<R, DV>& t, WaveTile<R, DV>& tile, int lane) {
     using W = WaveRegs<R, DV>;
@@ -119,7 +131,7 @@ __device__ __forceinline__ void store_tile(const WaveRegs<R, DV>& t, WaveTile<R,
 #pragma unroll
     for (int i = 0; i < W::KL; ++i) {
         const int c = lane + 64 * i;
-        *(float4*)(tile.k + (c / KC) * T::KS + (c % KC) * 4) = t.k[i];
+        *(float4*)(tile.k + (c / KC) * T::KS + kpos<R>(c / KC, c % KC) * 4) = t.k[i];
     }
 #pragma unroll
     for (int i = 0; i < W::VL; ++i) {
@@ -219,10 +231,11 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillP
 #pragma unroll
         for (int kb = 0; kb < 2; ++kb) {
             s[kb] = f32x4{0.f, 0.f, 0.f, 0.f};
-            const float* krow = tile.k + (kb * 16 + n) * KS + grp * RS;
+            const int kr = kb * 16 + n;
+            const float* krow = tile.k + kr * KS;
 #pragma unroll
             for (int s4 = 0; s4 < RS; s4 += 4) {
-                const float4 a = *(const float4*)(krow + s4);
+                const float4 a = *(const float4*)(krow + kpos<R>(kr, (grp * RS + s4) / 4) * 4);
                 s[kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.x, qreg[s4 + 0], s[kb], 0, 0, 0);
                 s[kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.y, qreg[s4 + 1], s[kb], 0, 0, 0);
                 s[kb] = __builtin_amdgcn_mfma_f32_16x16x4f32(a.z, qreg[s4 + 2], s[kb], 0, 0, 0);
