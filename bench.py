@@ -66,7 +66,8 @@ KERNEL_SOURCES = {"decode": "paper_2603_04427_amd/csrc/decode.hip",
                   "prefill_bf16": "paper_2603_04427_amd/csrc/prefill_bf16.hip",
                   "prefill_f32": "paper_2603_04427_amd/csrc/prefill_f32.hip",
                   "prefill_bwd": "paper_2603_04427_amd/csrc/prefill_bwd.hip",
-                  "append": "paper_2603_04427_amd/csrc/append.hip"}
+                  "append": "paper_2603_04427_amd/csrc/append.hip",
+                  "project": "paper_2603_04427_amd/csrc/project.hip"}
 
 
 def parse():
@@ -302,8 +303,8 @@ def projection_result(name, B, S, d_model, h_q, h_kv, r, dv, dev, steps, warmup,
         "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps, "dtype": "bf16",
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": acc.BF16_MFMA_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / acc.BF16_MFMA_PEAK_TFLOPS, 4),
-                     "traffic": None, "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5),
-                     "kernels": "project_kernel x 3 (q', k', v)"},
+                     "traffic": traffic_for(name, "project"), "algorithmic_flops": flops,
+                     "kernel_ms": round(ev * 1e3, 5), "kernels": "project_kernel x 3 (q', k', v)"},
     }
 
 
