@@ -734,7 +734,11 @@ static hipError_t by_group(const DecodeParams& p, int HG, int kf, bool paged, hi
         case 1: return by_layout<R, DV, 1>(p, kf, paged, st);
         case 2: return by_layout<R, DV, 2>(p, kf, paged, st);
         case 4: return by_layout<R, DV, 4>(p, kf, paged, st);
-        case 8: return by_layout<R, DV, 8>(p, kf, paged, st);
+        case 8:
+            // eight heads per workgroup only for r < 64; wider keys take four (their
+            // eight-head form would not fit the register budget)
+            if constexpr (R < 64) return by_layout<R, DV, 8>(p, kf, paged, st);
+            return hipErrorInvalidValue;
         default: return hipErrorInvalidValue;
     }
 }
