@@ -107,11 +107,23 @@ def traffic_for(workload: str, kind: str):
     return rec.get("bytes_per_call")
 
 
+MAX_TIMED_CALLS = 5000
+
+
+def plan_timed_calls(steps: int, one_call_s: float, min_timed_s: float) -> int:
+    """Timed calls for a line: ``steps``, raised (up to MAX_TIMED_CALLS) until
+    they cover ``min_timed_s`` at ``one_call_s`` per call; unchanged when
+    ``min_timed_s`` is 0 (the headline times exactly the steps it is given)."""
+    if min_timed_s <= 0:
+        return steps
+    return max(steps, min(MAX_TIMED_CALLS, int(min_timed_s / max(one_call_s, 1e-6)) + 1))
+
+
 def time_calls(calls, steps: int, warmup: int, min_timed_s: float = 0.0):
     """Warm up, then time ``steps`` calls (cycling through ``calls``).
 
     With ``min_timed_s`` > 0 (the secondary workloads; the headline line times
-    exactly the steps it is given) the timed calls are raised, up to 5000, until
+    exactly the steps it is given) the timed calls are raised, up to MAX_TIMED_CALLS, until
     they cover at least that many seconds, and as many extra warm-up calls as a
     quarter of them run first: a few calls of a kernel of some microseconds would
     otherwise time the host's launch gaps and the clock's ramp, not the kernel.
@@ -128,8 +140,7 @@ def time_calls(calls, steps: int, warmup: int, min_timed_s: float = 0.0):
         t = time.perf_counter()
         calls[0]()
         torch.cuda.synchronize()
-        one = max(time.perf_counter() - t, 1e-6)
-        steps = max(steps, min(5000, int(min_timed_s / one) + 1))
+        steps = plan_timed_calls(steps, time.perf_counter() - t, min_timed_s)
         for i in range(steps // 4):
             calls[i % n]()
         torch.cuda.synchronize()

@@ -89,3 +89,28 @@ def test_prefill_workload_flops_are_320_per_causal_pair():
     f = acc.prefill_flops(spec.batch, spec.h_q, spec.seq_q, spec.seq_k, spec.r, spec.d_v, spec.causal)
     pairs = spec.batch * spec.h_q * spec.seq_q * (spec.seq_q + 1) // 2
     assert f == pairs * 320
+
+
+def test_secondary_lines_time_at_least_their_minimum():
+    # the headline keeps exactly its steps
+    assert bench.plan_timed_calls(200, 32e-6, 0.0) == 200
+    # a 17 us kernel is timed for at least 50 ms, a 1 ms one for 51 calls
+    assert bench.plan_timed_calls(10, 17e-6, 0.05) == int(0.05 / 17e-6) + 1
+    assert bench.plan_timed_calls(10, 1e-3, 0.05) == 51
+    # never fewer than asked, never more than the cap
+    assert bench.plan_timed_calls(100, 1.0, 0.05) == 100
+    assert bench.plan_timed_calls(10, 1e-9, 0.05) == bench.MAX_TIMED_CALLS
+
+
+def test_every_traffic_record_names_a_known_kernel_source():
+    with open(bench.TRAFFIC_FILE) as f:
+        recs = json.load(f)
+    shas = {bench.source_sha(kind) for kind in bench.KERNEL_SOURCES}
+    for name, rec in recs.items():
+        assert len(rec["source_sha256"]) == 64, name
+        # a record is either current for one of the kernel sources or stale; a stale one reports no traffic
+        kind = next((k for k in bench.KERNEL_SOURCES if bench.source_sha(k) == rec["source_sha256"]), None)
+        if kind is None:
+            assert rec["source_sha256"] not in shas
+        else:
+            assert bench.traffic_for(name, kind) == rec["bytes_per_call"]
