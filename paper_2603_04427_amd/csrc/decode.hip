@@ -645,14 +645,17 @@ DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV) {
     while (G % hg) hg >>= 1;
     pl.heads_per_group = hg;
     const long pairs = (long)B * Hkv * (G / hg);
-    const long quanta = (max_ctx + 255) / 256;  // 256 tokens = one chunk per wave
+    // at least 512 tokens per split (four rounds at 32-token chunks): shorter
+    // splits leave each wave too few chunks to pipeline, and the last arriver
+    // more partials to merge, than their extra workgroups win back
+    const long quanta = (max_ctx + 511) / 512;
     const long target_groups = TK_DECODE_TARGET_GROUPS;  // workgroups to keep 256 CUs streaming
     long n_split = (target_groups + pairs - 1) / pairs;
     if (n_split > quanta) n_split = quanta;
     if (n_split > kMaxSplits) n_split = kMaxSplits;
     if (n_split < 1) n_split = 1;
     long split_quanta = quanta > 0 ? (quanta + n_split - 1) / n_split : 1;
-    pl.split_len = (int)(split_quanta * 256);
+    pl.split_len = (int)(split_quanta * 512);
     pl.n_split = max_ctx > 0 ? (int)((max_ctx + pl.split_len - 1) / pl.split_len) : 1;
     // One arrival counter per (sequence, head group). They are used only when
     // the context is split, which needs fewer than TARGET_GROUPS pairs (fewer

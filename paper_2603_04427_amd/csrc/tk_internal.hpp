@@ -37,7 +37,7 @@ struct DecodeParams {
 struct DecodePlan {
     int heads_per_group;  // query heads one workgroup serves (divides G, <= 8)
     int n_split;
-    int split_len;  // tokens per split, a multiple of 256 (planning: n_split = ceil(max_ctx / split_len))
+    int split_len;  // tokens per split, a multiple of 512 (planning: n_split = ceil(max_ctx / split_len))
     size_t counter_bytes;  // leading counter region of the workspace (256-byte multiple)
     size_t ws_bytes;
 };
