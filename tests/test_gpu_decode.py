@@ -2,7 +2,7 @@
 seeded inputs, at small sweep sizes (every output), at the full workload sizes
 in the launch configuration the benchmark times (every output of every
 sequence, i.i.d. and structured, for the batch-16, long-context paged, fp8-key
-and 4-bit-key steps),
+and 4-bit-key steps, and every output of the batch sweep's points),
 plus invariants that must hold at any size."""
 import pytest
 import torch
@@ -73,6 +73,20 @@ def test_mistral_decode_b16_full(name):
         out, ref = run_case(spec, structured)
         mx, rel = gate(out, ref, "bf16", f"{name} structured={structured}")
         say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
+
+
+@pytest.mark.parametrize("r", [32, 128])
+@pytest.mark.parametrize("B", [1, 2, 4, 8, 32])
+def test_batch_sweep_points_full(B, r):
+    """The decode batch sweep the benchmark reports (32/8 heads, context 4096, d_v
+    128; thin keys r 32 and standard keys r 128), built as the benchmark builds it,
+    with the split counts those batches get (8 splits at batches 1-4, 4 at 8, none
+    at 32): every output."""
+    from dataclasses import replace
+    spec = replace(WORKLOADS["mistral_decode_b16"], name=f"decode_b{B}_r{r}", batch=B, r=r)
+    out, ref = run_case(spec)
+    mx, rel = gate(out, ref, "bf16", spec.name)
+    say(f"  max-abs {mx:.2e} rel-L2 {rel:.2e}")
 
 
 @pytest.mark.parametrize("structured", [False, True])
