@@ -323,32 +323,38 @@ APPEND_CASES = {"cache_append_s8192": (4, 8192, "bf16"), "cache_append_fp8_s8192
                 "cache_append_int4_s8192": (4, 8192, "int4"), "cache_append_decode_b16": (16, 1, "bf16")}
 
 
-def append_result(name, B, Hkv, T, r, dv, kdt, dev, steps, warmup, min_timed_s=0.0):
+def append_result(name, B, Hkv, T, r, dv, kdt, dev, steps, warmup, min_timed_s=0.0, rotate=8):
     """tk_cache_append of T new tokens per (sequence, KV head) into a contiguous cache
-    with bf16, fp8 or 4-bit keys (``kdt``)."""
+    with bf16, fp8 or 4-bit keys (``kdt``). The timed calls cycle through ``rotate``
+    copies of the new rows and of the cache (each copy its own buffers), so that a
+    call's reads do not find the previous call's lines in the last-level cache."""
     import torch
     from paper_2603_04427_amd import prepare_cache_append
     from synth import normal, stream_key
 
-    kn = normal(stream_key(20, 0), B * Hkv * T * r, device=dev).view(B, Hkv, T, r).to(torch.bfloat16)
-    vn = normal(stream_key(20, 1), B * Hkv * T * dv, device=dev).view(B, Hkv, T, dv).to(torch.bfloat16)
+    kn0 = normal(stream_key(20, 0), B * Hkv * T * r, device=dev).view(B, Hkv, T, r).to(torch.bfloat16)
+    vn0 = normal(stream_key(20, 1), B * Hkv * T * dv, device=dev).view(B, Hkv, T, dv).to(torch.bfloat16)
     quant = kdt != "bf16"
-    kc = torch.zeros(B, Hkv, T, r // 2 if kdt == "int4" else r, dtype=torch.uint8 if quant else torch.bfloat16,
-                     device=dev)
-    vc = torch.zeros(B, Hkv, T, dv, dtype=torch.bfloat16, device=dev)
-    ks = torch.zeros(B, Hkv, T, dtype=torch.float32, device=dev) if quant else None
     pos = torch.zeros(B, dtype=torch.int32, device=dev)
-    call = prepare_cache_append(kn, vn, pos, kc, vc, k_scale=ks)
-    wall, ev, steps = time_calls([call], steps, warmup, min_timed_s)
+    bufs, calls = [], []
+    for i in range(max(1, rotate)):
+        kn, vn = (kn0, vn0) if i == 0 else (kn0.clone(), vn0.clone())
+        kc = torch.zeros(B, Hkv, T, r // 2 if kdt == "int4" else r, dtype=torch.uint8 if quant else torch.bfloat16,
+                         device=dev)
+        vc = torch.zeros(B, Hkv, T, dv, dtype=torch.bfloat16, device=dev)
+        ks = torch.zeros(B, Hkv, T, dtype=torch.float32, device=dev) if quant else None
+        bufs.append((kn, vn, kc, vc, ks))
+        calls.append(prepare_cache_append(kn, vn, pos, kc, vc, k_scale=ks))
+    wall, ev, steps = time_calls(calls, steps, warmup, min_timed_s)
     tokens = B * Hkv * T
     key_out = {"bf16": r * 2, "fp8": r + 4, "int4": r // 2 + 4}[kdt]
     nbytes = tokens * (r * 2 + dv * 2) + B * 4 + tokens * key_out + tokens * dv * 2
-    del kn, vn, kc, vc, ks, call
+    del kn0, vn0, bufs, calls
     torch.cuda.empty_cache()
     from paper_2603_04427_amd import accounting as acc
     return {
         "workload": name, "value": round(nbytes / wall / 1e9, 1), "unit": "GB/s",
-        "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps,
+        "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps, "rotate": max(1, rotate),
         "roofline": {"bound": "hbm", "achieved": round(nbytes / ev / 1e9, 1), "peak": acc.HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(nbytes / ev / 1e9 / acc.HBM_PEAK_GBS, 4),
                      "traffic": traffic_for(name, "append"), "algorithmic_bytes": nbytes,
@@ -512,7 +518,7 @@ def main():
         return
     if args.only and args.only.startswith("cache_append"):
         B, T, kdt = APPEND_CASES[args.only]
-        res = append_result(args.only, B, 8, T, 32, 128, kdt, dev, args.steps, args.warmup)
+        res = append_result(args.only, B, 8, T, 32, 128, kdt, dev, args.steps, args.warmup, rotate=args.rotate)
         print(json.dumps({"metric": "cache append HBM GB/s", "value": res["value"], "unit": "GB/s", "n_gpus": 1,
                           "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_call"],
                           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
@@ -590,7 +596,7 @@ def main():
         for name, (B, T, kdt) in APPEND_CASES.items():
             print(f"bench: timing {name}", file=sys.stderr, flush=True)
             appends.append(append_result(name, B, 8, T, 32, 128, kdt, dev, max(10, args.steps // 10),
-                                         args.warmup, SECONDARY_MIN_S))
+                                         args.warmup, SECONDARY_MIN_S, rotate=args.rotate))
     projections = []
     if not (args.only or args.no_secondary):
         for name, shape in PROJECTION_CASES.items():

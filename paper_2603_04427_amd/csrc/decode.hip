@@ -7,9 +7,10 @@
 //
 //  * Grouped-query packing: a workgroup serves all HG query heads that share a
 //    KV head, so each K/V byte crosses HBM once for HG heads.
-//  * Each wave streams 32- or 64-token chunks with 16-byte loads per lane, all
-//    of a chunk's K and V loads issued before any arithmetic: key rows tile the
-//    lanes (LPT lanes per row, one 16-byte slice each), value rows likewise.
+//  * Each wave streams 32- or 64-token chunks with 16-byte non-temporal loads
+//    per lane (each byte is read once per step), all of a chunk's K and V
+//    loads issued before any arithmetic: key rows tile the lanes (LPT lanes
+//    per row, one 16-byte slice each), value rows likewise.
 //    The waves of a workgroup take consecutive chunks (one round), and the
 //    splits of a (sequence, head group) take the rounds in turn, so together
 //    they read one contiguous stream of each cache rather than n_split
@@ -65,18 +66,23 @@ __device__ __forceinline__ float load_coherent(const float* p) {
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), 0, (int)bytes, 0x00020000);
 }
+// Cache policy of the cache stream's loads: the non-temporal bit (nt), the
+// hint that a line has no temporal reuse. Every K/V byte of a step is read
+// exactly once, so nothing is lost by not keeping the lines, and with the hint
+// the same loads run about a tenth faster (the results are bitwise the same).
+constexpr int kStreamPolicy = 2;
 __device__ __forceinline__ uint4 buffer_load16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0);
+    const u32x4 v = __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, kStreamPolicy);
     return make_uint4(v[0], v[1], v[2], v[3]);
 }
 __device__ __forceinline__ uint2 buffer_load8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0);
+    const u32x2 v = __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, kStreamPolicy);
     return make_uint2(v[0], v[1]);
 }
 __device__ __forceinline__ uint32_t buffer_load4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
-    return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+    return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, kStreamPolicy);
 }
 // A wave-uniform 32-bit load through the scalar cache (its own counter, so
 // waiting for it does not wait for the vector loads in flight).
