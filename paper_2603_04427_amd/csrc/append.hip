@@ -11,8 +11,9 @@
 //    even entry in the low nibble).
 //
 // The kernel is a plain stream: every thread moves one 16-byte slice of a key or
-// value row. The R / 8 threads holding one key row are consecutive lanes, so the
-// row maximum of the quantised paths is a butterfly over those lanes.
+// value row, read and written with non-temporal accesses. The R / 8 threads
+// holding one key row are consecutive lanes, so the row maximum of the
+// quantised paths is a butterfly over those lanes.
 #include "tk_device.hpp"
 #include "tk_internal.hpp"
 
@@ -25,6 +26,31 @@ namespace tk {
 namespace {
 
 constexpr int kAppendThreads = 256;
+
+// The new rows are read once and the cache rows written once, so both streams
+// carry the non-temporal hint (no temporal reuse): with it the same accesses
+// run about a tenth faster once neither stream can be served from a cache.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint4 load16_stream(const uint16_t* p) {
+    const u32x4 v = __builtin_nontemporal_load((const u32x4*)p);
+    return make_uint4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ void store16_stream(void* p, uint4 w) {
+    u32x4 v;
+    v[0] = w.x;
+    v[1] = w.y;
+    v[2] = w.z;
+    v[3] = w.w;
+    __builtin_nontemporal_store(v, (u32x4*)p);
+}
+__device__ __forceinline__ void store8_stream(void* p, uint32_t lo, uint32_t hi) {
+    u32x2 v;
+    v[0] = lo;
+    v[1] = hi;
+    __builtin_nontemporal_store(v, (u32x2*)p);
+}
+__device__ __forceinline__ void store4_stream(void* p, uint32_t w) { __builtin_nontemporal_store(w, (uint32_t*)p); }
 
 // OCP E4M3FN encoding of an fp32 value, rounded to nearest-even: bias 7, three
 // mantissa bits, subnormals with quantum 2^-9, largest finite 448, and no
@@ -83,7 +109,7 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendPara
     for (int i = first; i < p.T * KL; i += stride) {
         const int t = i / KL, slice = i % KL;
         const long row = cache_row(t);
-        const uint4 w = *(const uint4*)(kn + (size_t)i * 8);
+        const uint4 w = load16_stream(kn + (size_t)i * 8);
         if constexpr (KF != kKeyBF16) {
             const uint32_t wd[4] = {w.x, w.y, w.z, w.w};
             float f[8];
@@ -102,7 +128,7 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendPara
 #pragma unroll
                 for (int j = 0; j < 8; ++j) code[j >> 2] |= e4m3_rne(f[j] / scale) << (8 * (j & 3));
                 if (row >= 0) {
-                    *(uint2*)(p.kc + row * R + slice * 8) = make_uint2(code[0], code[1]);
+                    store8_stream(p.kc + row * R + slice * 8, code[0], code[1]);
                     if (slice == 0) p.ks[row] = scale;
                 }
             } else {
@@ -114,18 +140,18 @@ __global__ __launch_bounds__(kAppendThreads) void append_kernel(const AppendPara
                     code |= (uint32_t)((int)c + 8) << (4 * j);
                 }
                 if (row >= 0) {
-                    *(uint32_t*)(p.kc + row * (R / 2) + slice * 4) = code;
+                    store4_stream(p.kc + row * (R / 2) + slice * 4, code);
                     if (slice == 0) p.ks[row] = scale;
                 }
             }
         } else {
-            if (row >= 0) *(uint4*)(p.kc + (row * R + slice * 8) * 2) = w;
+            if (row >= 0) store16_stream(p.kc + (row * R + slice * 8) * 2, w);
         }
     }
     // value rows
     for (int i = first; i < p.T * VL; i += stride) {
         const long row = cache_row(i / VL);
-        if (row >= 0) *(uint4*)(p.vc + row * DV + (i % VL) * 8) = *(const uint4*)(vn + (size_t)i * 8);
+        if (row >= 0) store16_stream(p.vc + row * DV + (i % VL) * 8, load16_stream(vn + (size_t)i * 8));
     }
 }
 
