@@ -120,36 +120,53 @@ __global__ __launch_bounds__(proj_threads<BN>(), 1) void project_kernel(const Pr
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
     const int nk = p.K / kPBK;
+    // operand reads of k-step ks of the k-tile in `st`, and the products of one k-step
+    auto read_ops = [&](int st, int ks, bf16x8 (&a)[2], bf16x8 (&b)[T::kMB]) {
+        const uint16_t* ws = sm.w[st];
+        const uint16_t* xs = sm.x[st];
+        const int kc = 2 * ks + half;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(ws + sw(wn * 64 + i * 32 + col, kc));
+#pragma unroll
+        for (int j = 0; j < T::kMB; ++j) b[j] = *(const bf16x8*)(xs + sw(wm * (BM / 2) + j * 32 + col, kc));
+    };
+    auto products = [&](const bf16x8 (&a)[2], const bf16x8 (&b)[T::kMB]) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < T::kMB; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    };
     issue(0, 0);
     if (nk > 1) issue(1, 1);
     wait_copies<T::kCopies>(nk > 1);  // this lane's copies of k-tile 0 have landed
     __syncthreads();      // ... and everyone's
+    static_assert(kPBK == 32, "the pipeline below takes two 16-wide k-steps per k-tile");
+    // Software pipeline over the k-steps: the operands of the next k-step are
+    // read while the current one's products run, and the barrier that publishes
+    // k-tile kt + 1 sits between the two k-steps of k-tile kt, so that its first
+    // operand reads overlap the second k-step's products.
+    bf16x8 a0[2], b0[T::kMB], a1[2], b1[T::kMB];
+    read_ops(0, 0, a0, b0);
     int stage = 0;
-    for (int kt = 0; kt < nk; ++kt) {
-        // the stage k-tile kt + 2 goes to was last read in iteration kt - 1, which
-        // every wave has finished (the barrier at its end)
+    for (int kt = 0; kt + 1 < nk; ++kt) {
+        // the stage k-tile kt + 2 goes to was last read before the barrier that
+        // ended iteration kt - 1
         const bool ahead = kt + 2 < nk;
         if (ahead) issue(kt + 2, stage == 0 ? 2 : stage - 1);
-        const uint16_t* ws = sm.w[stage];
-        const uint16_t* xs = sm.x[stage];
-#pragma unroll
-        for (int ks = 0; ks < kPBK / 16; ++ks) {
-            const int kc = 2 * ks + half;
-            bf16x8 a[2], b[T::kMB];
-#pragma unroll
-            for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(ws + sw(wn * 64 + i * 32 + col, kc));
-#pragma unroll
-            for (int j = 0; j < T::kMB; ++j) b[j] = *(const bf16x8*)(xs + sw(wm * (BM / 2) + j * 32 + col, kc));
-#pragma unroll
-            for (int i = 0; i < 2; ++i)
-#pragma unroll
-                for (int j = 0; j < T::kMB; ++j)
-                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-        }
-        if (kt + 1 < nk) wait_copies<T::kCopies>(ahead);  // k-tile kt + 1 has landed (kt + 2 may still fly)
+        read_ops(stage, 1, a1, b1);
+        products(a0, b0);
+        const int next = stage == kStages - 1 ? 0 : stage + 1;
+        wait_copies<T::kCopies>(ahead);  // k-tile kt + 1 has landed (kt + 2 may still fly)
         __syncthreads();
-        stage = stage == kStages - 1 ? 0 : stage + 1;
+        read_ops(next, 0, a0, b0);
+        products(a1, b1);
+        stage = next;
     }
+    // the last k-tile
+    read_ops(stage, 1, a1, b1);
+    products(a0, b0);
+    products(a1, b1);
 
     // ---- epilogue: lane (col, half) of block (i, j) holds output columns
     // n0 + 8 g + 4 half + 0..3 (g = 0..3) of token m0 + col, rounded to bf16 and
