@@ -90,9 +90,17 @@ def parse():
     return ap.parse_args()
 
 
+# Headers every kernel source includes: a change to them changes the kernels too.
+SHARED_SOURCES = ("paper_2603_04427_amd/csrc/tk_device.hpp", "paper_2603_04427_amd/csrc/tk_internal.hpp")
+
+
 def source_sha(kind: str) -> str:
-    with open(os.path.join(ROOT, KERNEL_SOURCES[kind]), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """SHA-256 over the sources a kernel is built from: its own file, then the shared headers."""
+    h = hashlib.sha256()
+    for path in (KERNEL_SOURCES[kind],) + SHARED_SOURCES:
+        with open(os.path.join(ROOT, path), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def traffic_for(workload: str, kind: str):

@@ -352,14 +352,15 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? (R <= 32 ? 3 : 2) : 1) void pref
                         }
                 }
             }
-            // ---- row maxima and lazy rescale for each query block (the only branches)
+            // ---- row maxima (v_maximum3_f32) and lazy rescale for each query block
+            // (the only branches)
 #pragma unroll
             for (int qc = 0; qc < QC; ++qc) {
                 float mx = s[qc][0][0];
 #pragma unroll
-                for (int v = 1; v < 16; ++v) mx = fmaxf(mx, s[qc][0][v]);
+                for (int v = 1; v < 16; ++v) mx = max_f(mx, s[qc][0][v]);
 #pragma unroll
-                for (int v = 0; v < 16; ++v) mx = fmaxf(mx, s[qc][1][v]);
+                for (int v = 0; v < 16; ++v) mx = max_f(mx, s[qc][1][v]);
                 mx = xor32_max(mx);
                 const float mx2 = mx * c;
                 // each row moves its own reference; the branch is taken by the whole

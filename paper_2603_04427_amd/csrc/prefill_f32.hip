@@ -255,8 +255,8 @@ __global__ __launch_bounds__(kThreads, 1) void prefill_f32_kernel(const PrefillP
                     if (key > lim) s[kb][i] = -INFINITY;
                 }
         }
-        float mx = fmaxf(fmaxf(fmaxf(s[0][0], s[0][1]), fmaxf(s[0][2], s[0][3])),
-                         fmaxf(fmaxf(s[1][0], s[1][1]), fmaxf(s[1][2], s[1][3])));
+        float mx = max_f(max_f(max_f(s[0][0], s[0][1]), max_f(s[0][2], s[0][3])),
+                         max_f(max_f(s[1][0], s[1][1]), max_f(s[1][2], s[1][3])));
         mx = strided_max<16>(mx);  // over the query's 4 lane groups
         const float mx2 = mx * c;
         // each query moves its own reference only, when its maximum exceeds it by

@@ -89,13 +89,18 @@ __device__ __forceinline__ float xor32_sum(float x) {
     auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
     return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
+// Maximum of two floats, NaN-propagating: one v_maximum_f32 (or a third operand
+// of v_maximum3_f32) on gfx950, with no canonicalising copies of its inputs,
+// which fmaxf's NaN-ignoring rule needs for values of unknown origin (matrix
+// accumulators, lane exchanges). Equal to fmaxf whenever neither input is NaN.
+__device__ __forceinline__ float max_f(float a, float b) { return __builtin_elementwise_maximum(a, b); }
 __device__ __forceinline__ float xor16_max(float x) {
     auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    return max_f(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float xor32_max(float x) {
     auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+    return max_f(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 
 // Sum / max over aligned groups of N lanes (N a power of two <= 64); every lane
@@ -113,10 +118,10 @@ __device__ __forceinline__ float group_sum(float x) {
 
 template <int N>
 __device__ __forceinline__ float group_max(float x) {
-    if constexpr (N >= 2) x = fmaxf(x, dpp<kQuadXor1>(x));
-    if constexpr (N >= 4) x = fmaxf(x, dpp<kQuadXor2>(x));
-    if constexpr (N >= 8) x = fmaxf(x, dpp<kRowHalfMirror>(x));
-    if constexpr (N >= 16) x = fmaxf(x, dpp<kRowMirror>(x));
+    if constexpr (N >= 2) x = max_f(x, dpp<kQuadXor1>(x));
+    if constexpr (N >= 4) x = max_f(x, dpp<kQuadXor2>(x));
+    if constexpr (N >= 8) x = max_f(x, dpp<kRowHalfMirror>(x));
+    if constexpr (N >= 16) x = max_f(x, dpp<kRowMirror>(x));
     if constexpr (N >= 32) x = xor16_max(x);
     if constexpr (N >= 64) x = xor32_max(x);
     return x;
@@ -127,10 +132,10 @@ __device__ __forceinline__ float group_max(float x) {
 // inside each 16-lane row, then the 16- and 32-lane half swaps.
 template <int STRIDE>
 __device__ __forceinline__ float strided_max(float x) {
-    if constexpr (STRIDE <= 1) x = fmaxf(x, dpp<0x121>(x));
-    if constexpr (STRIDE <= 2) x = fmaxf(x, dpp<0x122>(x));
-    if constexpr (STRIDE <= 4) x = fmaxf(x, dpp<0x124>(x));
-    if constexpr (STRIDE <= 8) x = fmaxf(x, dpp<0x128>(x));
+    if constexpr (STRIDE <= 1) x = max_f(x, dpp<0x121>(x));
+    if constexpr (STRIDE <= 2) x = max_f(x, dpp<0x122>(x));
+    if constexpr (STRIDE <= 4) x = max_f(x, dpp<0x124>(x));
+    if constexpr (STRIDE <= 8) x = max_f(x, dpp<0x128>(x));
     if constexpr (STRIDE <= 16) x = xor16_max(x);
     if constexpr (STRIDE <= 32) x = xor32_max(x);
     return x;
