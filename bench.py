@@ -10,8 +10,10 @@ that the 168 MB step does not run out of the 256 MB last-level cache.
 The JSON line reports, besides the contract fields:
   roofline      achieved algorithmic GB/s of the decode kernel (HIP events on
                 the launch stream, averaged over the timed calls) against
-                8 TB/s, and the HBM traffic per call from rocprofv3 counters
-                when they were taken on the current kernel source;
+                8 TB/s, the median and minimum of single calls timed one by
+                one after the timed region, and the HBM traffic per call from
+                rocprofv3 counters when they were taken on the current kernel
+                sources;
   cpu_baseline  the fp64 oracle on the host cores, on a bounded sample of the
                 same workload (not an optimisation target), with the CPU model,
                 usable cores and OMP_NUM_THREADS; each secondary workload
@@ -115,7 +117,18 @@ def traffic_for(workload: str, kind: str):
     return rec.get("bytes_per_call")
 
 
+def event_ms(ev: float, one) -> dict:
+    """Time fields of a roofline record: the mean over the back-to-back timed calls
+    (the denominator of ``achieved``), and the median and minimum of single calls,
+    each between its own events. A single call's figure also holds the gap the
+    event between two calls leaves (the next launch no longer overlaps the end of
+    the previous kernel), so it sits above the mean for short kernels."""
+    return {"kernel_ms": round(ev * 1e3, 5), "single_call_ms_median": round(one[0] * 1e3, 5),
+            "single_call_ms_min": round(one[1] * 1e3, 5)}
+
+
 MAX_TIMED_CALLS = 5000
+PER_CALL_MAX = 200  # single calls timed one by one after the timed region
 
 
 def plan_timed_calls(steps: int, one_call_s: float, min_timed_s: float) -> int:
@@ -136,9 +149,12 @@ def time_calls(calls, steps: int, warmup: int, min_timed_s: float = 0.0):
     quarter of them run first: a few calls of a kernel of some microseconds would
     otherwise time the host's launch gaps and the clock's ramp, not the kernel.
 
-    Returns (wall seconds per step, event seconds per step, timed calls). The
-    wall clock is bracketed by device synchronisation; the events sit on the
-    launch stream."""
+    Returns (wall seconds per step, event seconds per step, timed calls,
+    (median, min) seconds of single calls). The wall clock is bracketed by device
+    synchronisation; the events sit on the launch stream. After the timed region,
+    as many calls again (at most PER_CALL_MAX) are timed one by one, an event
+    recorded between consecutive calls, for the median and the minimum of a
+    single call."""
     import torch
     n = len(calls)
     for i in range(warmup):
@@ -162,7 +178,15 @@ def time_calls(calls, steps: int, warmup: int, min_timed_s: float = 0.0):
     torch.cuda.synchronize()
     wall = (time.perf_counter() - t0) / steps
     ev = e0.elapsed_time(e1) / 1e3 / steps
-    return wall, ev, steps
+    m = min(steps, PER_CALL_MAX)
+    marks = [torch.cuda.Event(enable_timing=True) for _ in range(m + 1)]
+    marks[0].record(st)
+    for i in range(m):
+        calls[i % n]()
+        marks[i + 1].record(st)
+    torch.cuda.synchronize()
+    one = sorted(marks[i].elapsed_time(marks[i + 1]) / 1e3 for i in range(m))
+    return wall, ev, steps, (one[m // 2], one[0])
 
 
 def decode_setup(spec, dev, rotate: int):
@@ -187,7 +211,7 @@ def decode_setup(spec, dev, rotate: int):
 
 def decode_result(name, spec, calls, steps, warmup, min_timed_s=0.0):
     from paper_2603_04427_amd import accounting as acc
-    wall, ev, steps = time_calls(calls, steps, warmup, min_timed_s)
+    wall, ev, steps, one = time_calls(calls, steps, warmup, min_timed_s)
     nbytes = acc.decode_bytes(spec.lens, spec.h_q, spec.h_kv, spec.r, spec.d_v, spec.k_dtype,
                               spec.blocks_per_seq if spec.paged else None)
     achieved = nbytes / ev / 1e9
@@ -197,7 +221,7 @@ def decode_result(name, spec, calls, steps, warmup, min_timed_s=0.0):
         "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": acc.HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / acc.HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "algorithmic_bytes": nbytes, "kernel_ms": round(ev * 1e3, 5)},
+                     "algorithmic_bytes": nbytes, **event_ms(ev, one)},
     }
 
 
@@ -209,7 +233,7 @@ def prefill_result(name, spec, dev, steps, warmup, min_timed_s=0.0):
 
     p = make_prefill(spec, device=dev)
     call = prepare_prefill(p["q"], p["k"], p["v"], causal=spec.causal, scale=spec.softmax_scale)
-    wall, ev, steps = time_calls([call], steps, warmup, min_timed_s)
+    wall, ev, steps, one = time_calls([call], steps, warmup, min_timed_s)
     flops = acc.prefill_flops(spec.batch, spec.h_q, spec.seq_q, spec.seq_k, spec.r, spec.d_v, spec.causal)
     peak = acc.BF16_MFMA_PEAK_TFLOPS if spec.dtype == "bf16" else acc.FP32_MFMA_PEAK_TFLOPS
     achieved = flops / ev / 1e12
@@ -221,7 +245,7 @@ def prefill_result(name, spec, dev, steps, warmup, min_timed_s=0.0):
         "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps, "dtype": spec.dtype,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": traffic_for(name, kind),
-                     "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5)},
+                     "algorithmic_flops": flops, **event_ms(ev, one)},
     }
 
 
@@ -238,7 +262,7 @@ def backward_result(name, spec, dev, steps, warmup, min_timed_s=0.0):
     o, lse = tk_attn_prefill_lse(p["q"], p["k"], p["v"], causal=spec.causal, scale=spec.softmax_scale)
     call = prepare_prefill_backward(p["q"], p["k"], p["v"], o, do, lse, causal=spec.causal,
                                     scale=spec.softmax_scale)
-    wall, ev, steps = time_calls([call], steps, warmup, min_timed_s)
+    wall, ev, steps, one = time_calls([call], steps, warmup, min_timed_s)
     flops = acc.prefill_backward_flops(spec.batch, spec.h_q, spec.seq_q, spec.seq_k, spec.r, spec.d_v,
                                        spec.causal)
     peak = acc.BF16_MFMA_PEAK_TFLOPS
@@ -250,7 +274,7 @@ def backward_result(name, spec, dev, steps, warmup, min_timed_s=0.0):
         "ms_per_call": round(wall * 1e3, 5), "timed_calls": steps, "dtype": spec.dtype,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
                      "frac": round(achieved / peak, 4), "traffic": traffic_for(name, "prefill_bwd"),
-                     "algorithmic_flops": flops, "kernel_ms": round(ev * 1e3, 5),
+                     "algorithmic_flops": flops, **event_ms(ev, one),
                      "kernels": "bwd_dq_kernel + bwd_dkdv_kernel"},
     }
 
@@ -312,7 +336,7 @@ def projection_result(name, B, S, d_model, h_q, h_kv, r, dv, dev, steps, warmup,
     def step():
         for c in calls:
             c()
-    wall, ev, steps = time_calls([step], steps, warmup, min_timed_s)
+    wall, ev, steps, one = time_calls([step], steps, warmup, min_timed_s)
     flops = 2 * B * S * d_model * cols
     achieved = flops / ev / 1e12
     del x, calls
@@ -323,7 +347,7 @@ def projection_result(name, B, S, d_model, h_q, h_kv, r, dv, dev, steps, warmup,
         "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": acc.BF16_MFMA_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / acc.BF16_MFMA_PEAK_TFLOPS, 4),
                      "traffic": traffic_for(name, "project"), "algorithmic_flops": flops,
-                     "kernel_ms": round(ev * 1e3, 5), "kernels": "project_kernel x 3 (q', k', v)"},
+                     **event_ms(ev, one), "kernels": "project_kernel x 3 (q', k', v)"},
     }
 
 
@@ -353,7 +377,7 @@ def append_result(name, B, Hkv, T, r, dv, kdt, dev, steps, warmup, min_timed_s=0
         ks = torch.zeros(B, Hkv, T, dtype=torch.float32, device=dev) if quant else None
         bufs.append((kn, vn, kc, vc, ks))
         calls.append(prepare_cache_append(kn, vn, pos, kc, vc, k_scale=ks))
-    wall, ev, steps = time_calls(calls, steps, warmup, min_timed_s)
+    wall, ev, steps, one = time_calls(calls, steps, warmup, min_timed_s)
     tokens = B * Hkv * T
     key_out = {"bf16": r * 2, "fp8": r + 4, "int4": r // 2 + 4}[kdt]
     nbytes = tokens * (r * 2 + dv * 2) + B * 4 + tokens * key_out + tokens * dv * 2
@@ -366,7 +390,7 @@ def append_result(name, B, Hkv, T, r, dv, kdt, dev, steps, warmup, min_timed_s=0
         "roofline": {"bound": "hbm", "achieved": round(nbytes / ev / 1e9, 1), "peak": acc.HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(nbytes / ev / 1e9 / acc.HBM_PEAK_GBS, 4),
                      "traffic": traffic_for(name, "append"), "algorithmic_bytes": nbytes,
-                     "kernel_ms": round(ev * 1e3, 5)},
+                     **event_ms(ev, one)},
     }
 
 

@@ -114,3 +114,8 @@ def test_every_traffic_record_names_a_known_kernel_source():
             assert rec["source_sha256"] not in shas
         else:
             assert bench.traffic_for(name, kind) == rec["bytes_per_call"]
+
+
+def test_event_fields_carry_mean_median_and_min():
+    rec = bench.event_ms(30e-6, (29.5e-6, 28.25e-6))
+    assert rec == {"kernel_ms": 0.03, "single_call_ms_median": 0.0295, "single_call_ms_min": 0.02825}
