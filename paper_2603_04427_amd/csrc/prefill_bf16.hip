@@ -133,7 +133,11 @@ __device__ __forceinline__ void load_tile(const TileLanes<R, DV, NT>& tl, uint16
     // offset. The copy's vector offset is unsigned, so here every copy keeps the
     // tile's own base and adds its stride to the offset: the clamped offset then
     // stays non-negative even where `last` lies above copy i's first row.
-    const int last = Sk - base - 1;
+    int last = Sk - base - 1;
+    // opaque to the loop's induction analysis: otherwise the compiler keeps the
+    // clamped offsets as induction variables updated on every tile, though
+    // only a ragged last tile uses them
+    asm volatile("" : "+s"(last));
 #pragma unroll
     for (int i = 0; i < T::KL; ++i) {
         if (T::KC % NT != 0 && wave_base + i * NT >= T::KC) break;
