@@ -485,17 +485,60 @@ def copy_calibration(mib: int, dev):
     print(json.dumps({"copy_calibration_bytes_read": n, "copy_calibration_bytes_written": n, "launches": 3}))
 
 
+PROBE_LIB = os.path.join(ROOT, "paper_2603_04427_amd", "libtkprobe.so")
+
+
+def stream_read_rates(dev, nbytes: int = 167936064, copies: int = 8, grid: int = 256, reps: int = 50) -> dict:
+    """A plain streaming read of ``nbytes`` (the batch-16 decode step's bytes) with
+    the probe kernel (libtkprobe: ``grid`` workgroups, four 16-byte loads in flight
+    per lane, grid-stride), cycling through ``copies`` buffers so that no read is
+    served from the last-level cache; with ordinary and with non-temporal loads.
+    The mean over ``reps`` back-to-back launches, from HIP events."""
+    import ctypes
+    import torch
+    lib = ctypes.CDLL(PROBE_LIB)  # built beside libtkattn; a missing probe is an error
+    lib.tkprobe_threads.restype = ctypes.c_int
+    lib.tkprobe_stream_read.restype = ctypes.c_int
+    lib.tkprobe_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int,
+                                        ctypes.c_int, ctypes.c_void_p]
+    n = nbytes // 16 * 16
+    bufs = [torch.ones(n, dtype=torch.uint8, device=dev) for _ in range(copies)]
+    sink = torch.empty(grid * lib.tkprobe_threads(), dtype=torch.int32, device=dev)
+    st = torch.cuda.current_stream()
+    out = {"bytes": n, "copies": copies, "workgroups": grid, "threads": lib.tkprobe_threads()}
+    for nt, key in ((0, "GBps"), (1, "non_temporal_GBps")):
+        def call(i):
+            rc = lib.tkprobe_stream_read(ctypes.c_void_p(bufs[i % copies].data_ptr()), n,
+                                         ctypes.c_void_p(sink.data_ptr()), grid, nt, ctypes.c_void_p(st.cuda_stream))
+            if rc != 0:
+                raise RuntimeError(f"tkprobe_stream_read returned {rc}")
+        for i in range(2 * copies):
+            call(i)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(st)
+        for i in range(reps):
+            call(i)
+        e1.record(st)
+        torch.cuda.synchronize()
+        out[key] = round(n / (e0.elapsed_time(e1) / 1e3 / reps) / 1e9, 1)
+    del bufs, sink
+    torch.cuda.empty_cache()
+    return out
+
+
 def device_context(dev):
     """What the part reports and plain streaming rates measured on it, as context
     for the roofline fractions (which use the published peaks): CU count and
-    architecture, the engine clock levels the driver lists, and the rates of
-    torch's own kernels for a read-only sum over 2 GiB and a 1 GiB copy (best of
-    5, HIP events). These are library kernels, not the part's ceiling."""
+    architecture, the engine clock levels the driver lists, a plain streaming
+    read of the decode step's size by a probe kernel (``stream_read``), and the
+    rates of torch's own kernels for a read-only sum over 2 GiB and a 1 GiB copy
+    (best of 5, HIP events), which are library kernels, not the part's ceiling."""
     import glob
     import torch
     props = torch.cuda.get_device_properties(dev)
     ctx = {"name": props.name, "arch": props.gcnArchName, "cus": props.multi_processor_count,
-           "sclk_mhz_levels": None, "torch_sum_read_GBps": None, "torch_copy_GBps": None}
+           "sclk_mhz_levels": None, "stream_read": None, "torch_sum_read_GBps": None, "torch_copy_GBps": None}
     for path in sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk")):
         try:
             with open(path) as f:
@@ -520,6 +563,7 @@ def device_context(dev):
             t.append(e0.elapsed_time(e1) / 1e3)
         return round(nbytes / min(t) / 1e9, 1)
 
+    ctx["stream_read"] = stream_read_rates(dev)
     x = torch.ones((2 << 30) // 4, dtype=torch.float32, device=dev)
     ctx["torch_sum_read_GBps"] = best(lambda: x.sum(), x.numel() * 4)
     del x

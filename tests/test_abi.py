@@ -242,3 +242,23 @@ def append(**kw):
 ])
 def test_append_validation(kw, status):
     assert append(**kw) == status
+
+
+def test_stream_probe_library_loads_and_rejects_bad_arguments():
+    """The benchmark's streaming-read probe (a separate library, not the attention
+    ABI) loads and rejects bad arguments before any HIP call."""
+    path = os.path.join(ROOT, "paper_2603_04427_amd", "libtkprobe.so")
+    if not os.path.exists(path):
+        pytest.skip("probe library not built")
+    lib = ctypes.CDLL(path)
+    lib.tkprobe_threads.restype = ctypes.c_int
+    assert lib.tkprobe_threads() == 512
+    f = lib.tkprobe_stream_read
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_int, ctypes.c_int, ctypes.c_void_p]
+    assert f(None, 4096, P, 256, 0, None) == 1        # no buffer
+    assert f(P, 4096, None, 256, 0, None) == 1        # no sink
+    assert f(P, 4100, P, 256, 0, None) == 1           # not a multiple of 16 bytes
+    assert f(P_ODD, 4096, P, 256, 0, None) == 1       # misaligned
+    assert f(P, 4096, P, 0, 1, None) == 1             # empty grid
+    assert f(P, 0, P, 256, 1, None) == 1              # nothing to read
