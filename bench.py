@@ -92,14 +92,22 @@ def parse():
     return ap.parse_args()
 
 
-# Headers every kernel source includes: a change to them changes the kernels too.
+# Other units built from a kernel's file (decode_short.hip compiles decode.hip's
+# eight-wave kernels), and the headers every kernel source includes: a change to
+# any of them changes the kernels too.
+EXTRA_SOURCES = {"decode": ("paper_2603_04427_amd/csrc/decode_short.hip",)}
 SHARED_SOURCES = ("paper_2603_04427_amd/csrc/tk_device.hpp", "paper_2603_04427_amd/csrc/tk_internal.hpp")
 
 
+def kernel_source_files(kind: str) -> tuple:
+    """The files a kernel is built from, in the order source_sha hashes them."""
+    return (KERNEL_SOURCES[kind],) + EXTRA_SOURCES.get(kind, ()) + SHARED_SOURCES
+
+
 def source_sha(kind: str) -> str:
-    """SHA-256 over the sources a kernel is built from: its own file, then the shared headers."""
+    """SHA-256 over the sources a kernel is built from (kernel_source_files)."""
     h = hashlib.sha256()
-    for path in (KERNEL_SOURCES[kind],) + SHARED_SOURCES:
+    for path in kernel_source_files(kind):
         with open(os.path.join(ROOT, path), "rb") as f:
             h.update(f.read())
     return h.hexdigest()

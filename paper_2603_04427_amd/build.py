@@ -22,7 +22,7 @@ PROBE_LIB = os.path.join(PKG, "libtkprobe.so")
 PROBE_SOURCE = "stream_probe.hip"
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["api.cpp", "decode.hip", "prefill_bf16.hip", "prefill_f32.hip", "prefill_bwd.hip", "append.hip", "project.hip"]
+SOURCES = ["api.cpp", "decode.hip", "decode_short.hip", "prefill_bf16.hip", "prefill_f32.hip", "prefill_bwd.hip", "append.hip", "project.hip"]
 FLAGS = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-I" + INCLUDE, "-I" + CSRC,
          # packed fp32 arithmetic stays off: ordinary fp32 code only
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

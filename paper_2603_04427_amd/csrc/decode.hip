@@ -45,11 +45,12 @@
 
 namespace tk {
 
-#ifndef TK_DECODE_WAVES
-#define TK_DECODE_WAVES 4
-#endif
-constexpr int kDecodeWaves = TK_DECODE_WAVES;  // waves per workgroup, each streaming its own chunks
-constexpr int kDecodeThreads = 64 * kDecodeWaves;
+// Waves per workgroup, each streaming its own chunks: 4, or 8 when each wave
+// would otherwise get at most four chunks of its split (short streams, where
+// latency rather than bandwidth sets the time).
+constexpr int kDecodeWavesLong = 4;
+constexpr int kDecodeWavesShort = 8;
+constexpr int kShortRounds = 4;
 constexpr int kMaxSplits = 1024;
 constexpr size_t kCounterRegionBytes = 2 * TK_DECODE_TARGET_GROUPS * sizeof(unsigned);
 static_assert(kCounterRegionBytes % 256 == 0, "the partials after the counters stay 256-byte aligned");
@@ -360,15 +361,17 @@ __device__ __forceinline__ void process_chunk(Chunk<R, DV, HG, KF, CH>& c, int n
     wave_lds_sync();
 }
 
-// Two workgroups per CU where the registers allow it; 4-bit keys with eight
-// heads per workgroup (their unpacked query slices are twice as wide) take the
-// whole register file of one.
-template <int HG, int KF>
-constexpr int decode_min_blocks() { return KF == kKeyInt4 && HG == 8 ? 1 : 2; }
+// Two four-wave workgroups per CU where the registers allow it; 4-bit keys with
+// eight heads per workgroup (their unpacked query slices are twice as wide), and
+// every eight-wave form, take the whole register file of one.
+template <int HG, int KF, int NW>
+constexpr int decode_min_blocks() { return NW == kDecodeWavesLong && !(KF == kKeyInt4 && HG == 8) ? 2 : 1; }
 
-template <int R, int DV, int HG, int KF, bool PAGED>
-__global__ __launch_bounds__(kDecodeThreads, (decode_min_blocks<HG, KF>())) void decode_split_kernel(
+template <int R, int DV, int HG, int KF, bool PAGED, int NW>
+__global__ __launch_bounds__(64 * NW, (decode_min_blocks<HG, KF, NW>())) void decode_split_kernel(
     const DecodeParams p) {
+    constexpr int kDecodeWaves = NW;
+    constexpr int kDecodeThreads = 64 * NW;
     constexpr int CH = DecodeSchedule<R, DV, HG, KF>::CH;
     constexpr bool PIPE = DecodeSchedule<R, DV, HG, KF>::PIPE;
     using S = DecodeShape<R, DV, HG, KF, CH>;
@@ -642,6 +645,7 @@ __global__ __launch_bounds__(kDecodeThreads, (decode_min_blocks<HG, KF>())) void
     if (threadIdx.x == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+#ifndef TK_DECODE_SHORT_UNIT
 // ------------------------------------------------------------------ planning
 
 DecodePlan plan_decode(int B, int Hq, int Hkv, int max_ctx, int DV) {
@@ -713,63 +717,113 @@ tk_status decode_scratch(hipStream_t stream, void** ptr) {
     return TK_OK;
 }
 
+#endif  // TK_DECODE_SHORT_UNIT
+
 // ------------------------------------------------------------------ dispatch
+//
+// The dispatch chain is instantiated twice: for four-wave workgroups in this
+// file, and for eight-wave ones in decode_short.hip, which includes this file
+// with TK_DECODE_SHORT_UNIT defined (the two sets then compile in parallel).
 
-template <int R, int DV, int HG, int KF, bool PAGED>
+// Eight-wave launches (decode_short.hip).
+tk_status launch_decode_short(const DecodeParams& p, int R, int DV, int HG, int key_format, bool paged,
+                              hipStream_t st);
+
+// Whether a layout has an eight-wave form: not 4-bit keys with eight heads per
+// workgroup, which need the whole register file of a SIMD for one wave.
+template <int HG, int KF>
+constexpr bool has_short_form() { return !(KF == kKeyInt4 && HG == 8); }
+
+// Four-wave workgroups, unless they would give each wave at most kShortRounds
+// chunks of its split (small batches at short contexts): then eight. The choice
+// depends only on the shapes, so a shape's output stays bitwise reproducible.
+template <int NW, int R, int DV, int HG, int KF>
+static bool use_short(const DecodeParams& p) {
+    if constexpr (NW != kDecodeWavesLong || !has_short_form<HG, KF>()) {
+        return false;
+    } else {
+        constexpr int CH = DecodeSchedule<R, DV, HG, KF>::CH;
+        const long rounds = ((long)p.max_ctx + kDecodeWavesLong * CH - 1) / (kDecodeWavesLong * CH);
+        return (rounds + p.n_split - 1) / p.n_split <= kShortRounds;
+    }
+}
+
+template <int NW, int R, int DV, int HG, int KF, bool PAGED>
 static hipError_t run(const DecodeParams& p, hipStream_t st) {
-    dim3 grid(p.n_split, p.Hkv * (p.G / HG), p.B);
-    hipLaunchKernelGGL((decode_split_kernel<R, DV, HG, KF, PAGED>), grid, dim3(kDecodeThreads), 0, st, p);
-    return hipGetLastError();
+    if constexpr (NW == kDecodeWavesShort && !has_short_form<HG, KF>()) {
+        return hipErrorInvalidValue;  // never chosen (use_short), and not built
+    } else {
+        if (use_short<NW, R, DV, HG, KF>(p)) {
+            const tk_status s = launch_decode_short(p, R, DV, HG, KF, PAGED, st);
+            return s == TK_OK ? hipSuccess : (s == TK_ERR_UNSUPPORTED ? hipErrorInvalidValue : hipErrorLaunchFailure);
+        }
+        const dim3 grid(p.n_split, p.Hkv * (p.G / HG), p.B);
+        hipLaunchKernelGGL((decode_split_kernel<R, DV, HG, KF, PAGED, NW>), grid, dim3(64 * NW), 0, st, p);
+        return hipGetLastError();
+    }
 }
 
-template <int R, int DV, int HG, int KF>
+template <int NW, int R, int DV, int HG, int KF>
 static hipError_t by_paging(const DecodeParams& p, bool paged, hipStream_t st) {
-    return paged ? run<R, DV, HG, KF, true>(p, st) : run<R, DV, HG, KF, false>(p, st);
+    return paged ? run<NW, R, DV, HG, KF, true>(p, st) : run<NW, R, DV, HG, KF, false>(p, st);
 }
 
-template <int R, int DV, int HG>
+template <int NW, int R, int DV, int HG>
 static hipError_t by_layout(const DecodeParams& p, int kf, bool paged, hipStream_t st) {
     switch (kf) {
-        case kKeyBF16: return by_paging<R, DV, HG, kKeyBF16>(p, paged, st);
-        case kKeyE4M3: return by_paging<R, DV, HG, kKeyE4M3>(p, paged, st);
-        case kKeyInt4: return by_paging<R, DV, HG, kKeyInt4>(p, paged, st);
+        case kKeyBF16: return by_paging<NW, R, DV, HG, kKeyBF16>(p, paged, st);
+        case kKeyE4M3: return by_paging<NW, R, DV, HG, kKeyE4M3>(p, paged, st);
+        case kKeyInt4: return by_paging<NW, R, DV, HG, kKeyInt4>(p, paged, st);
         default: return hipErrorInvalidValue;
     }
 }
 
-template <int R, int DV>
+template <int NW, int R, int DV>
 static hipError_t by_group(const DecodeParams& p, int HG, int kf, bool paged, hipStream_t st) {
     switch (HG) {
-        case 1: return by_layout<R, DV, 1>(p, kf, paged, st);
-        case 2: return by_layout<R, DV, 2>(p, kf, paged, st);
-        case 4: return by_layout<R, DV, 4>(p, kf, paged, st);
+        case 1: return by_layout<NW, R, DV, 1>(p, kf, paged, st);
+        case 2: return by_layout<NW, R, DV, 2>(p, kf, paged, st);
+        case 4: return by_layout<NW, R, DV, 4>(p, kf, paged, st);
         case 8:
             // eight heads per workgroup only for r < 64; wider keys take four (their
             // eight-head form would not fit the register budget)
-            if constexpr (R < 64) return by_layout<R, DV, 8>(p, kf, paged, st);
+            if constexpr (R < 64) return by_layout<NW, R, DV, 8>(p, kf, paged, st);
             return hipErrorInvalidValue;
         default: return hipErrorInvalidValue;
     }
 }
 
-template <int R>
+template <int NW, int R>
 static hipError_t by_dv(const DecodeParams& p, int DV, int HG, int kf, bool paged, hipStream_t st) {
-    if (DV == 64) return by_group<R, 64>(p, HG, kf, paged, st);
-    if (DV == 128) return by_group<R, 128>(p, HG, kf, paged, st);
+    if (DV == 64) return by_group<NW, R, 64>(p, HG, kf, paged, st);
+    if (DV == 128) return by_group<NW, R, 128>(p, HG, kf, paged, st);
     return hipErrorInvalidValue;
 }
 
-tk_status launch_decode(const DecodeParams& p, int R, int DV, int HG, int key_format, bool paged, hipStream_t st) {
+template <int NW>
+static tk_status launch_waves(const DecodeParams& p, int R, int DV, int HG, int key_format, bool paged,
+                              hipStream_t st) {
     hipError_t e;
     switch (R) {
-        case 16: e = by_dv<16>(p, DV, HG, key_format, paged, st); break;
-        case 32: e = by_dv<32>(p, DV, HG, key_format, paged, st); break;
-        case 64: e = by_dv<64>(p, DV, HG, key_format, paged, st); break;
-        case 128: e = by_dv<128>(p, DV, HG, key_format, paged, st); break;
+        case 16: e = by_dv<NW, 16>(p, DV, HG, key_format, paged, st); break;
+        case 32: e = by_dv<NW, 32>(p, DV, HG, key_format, paged, st); break;
+        case 64: e = by_dv<NW, 64>(p, DV, HG, key_format, paged, st); break;
+        case 128: e = by_dv<NW, 128>(p, DV, HG, key_format, paged, st); break;
         default: return TK_ERR_UNSUPPORTED;
     }
     if (e == hipErrorInvalidValue) return TK_ERR_UNSUPPORTED;
     return e == hipSuccess ? TK_OK : TK_ERR_HIP;
 }
+
+#ifdef TK_DECODE_SHORT_UNIT
+tk_status launch_decode_short(const DecodeParams& p, int R, int DV, int HG, int key_format, bool paged,
+                              hipStream_t st) {
+    return launch_waves<kDecodeWavesShort>(p, R, DV, HG, key_format, paged, st);
+}
+#else
+tk_status launch_decode(const DecodeParams& p, int R, int DV, int HG, int key_format, bool paged, hipStream_t st) {
+    return launch_waves<kDecodeWavesLong>(p, R, DV, HG, key_format, paged, st);
+}
+#endif
 
 }  // namespace tk
