@@ -35,6 +35,8 @@
 #include "tk_device.hpp"
 #include "tk_internal.hpp"
 
+#include <type_traits>
+
 #include <math.h>
 
 namespace tk {
@@ -313,8 +315,11 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? (R <= 32 ? 3 : 2) : 1) void pref
     __builtin_amdgcn_s_waitcnt(0x0F70);
     __syncthreads();
 
-    for (int t = 0; t < ntiles; ++t) {
-        const int cur = t & 1;
+    // the loop over key tiles, two tiles per iteration, so that the double buffer
+    // each tile uses is a compile-time constant and its LDS addresses take
+    // immediate offsets
+    auto tile_step = [&](auto cur_c, int t) {
+        constexpr int cur = decltype(cur_c)::value;
         const int base = t * kBN;
         if (t + 1 < ntiles) load_tile<R, DV, NT>(tl, sm.k[cur ^ 1], sm.v[cur ^ 1], kg, vg, base + kBN, p.Sk, wave);
 
@@ -432,7 +437,13 @@ __global__ __launch_bounds__(64 * NW, QC == 1 ? (R <= 32 ? 3 : 2) : 1) void pref
 
         if (t + 1 < ntiles) wait_loads();  // this wave's part of the next tile has landed
         __syncthreads();
+    };
+    int t = 0;
+    for (; t + 1 < ntiles; t += 2) {
+        tile_step(std::integral_constant<int, 0>{}, t);
+        tile_step(std::integral_constant<int, 1>{}, t + 1);
     }
+    if (t < ntiles) tile_step(std::integral_constant<int, 0>{}, t);
 
     // ---- epilogue: normalise and store bf16 rows (and, when asked, the row's
     // log-sum-exp: the reference maximum plus log2 of the sum, in natural log)
