@@ -194,24 +194,43 @@ __global__ __launch_bounds__(proj_threads<BN>(), 1) void project_kernel(const Pr
 
 }  // namespace
 
-// 256 x 256 tiles (8 waves, one workgroup per CU) when they give every CU a
-// tile; otherwise 128 x 128 tiles (4 waves, two workgroups per CU), so that
-// narrow projections (a few KV heads of thin keys) and short sequences still
-// spread over the part.
-static bool big_tiles(long M, long N) { return ((M + 255) / 256) * ((N + 255) / 256) >= 256; }
+// Tile shape of a call, the largest that still gives every CU a workgroup:
+// 256 x 256 (8 waves of 64 columns x 128 tokens, one workgroup per CU); else
+// 256 columns x 128 tokens (8 waves of 64 x 64), which serves the narrow
+// thin-key projection (a few KV heads of r columns) over long inputs with the
+// token rows read once; else 128 x 128 (4 waves, two workgroups per CU), so that
+// short sequences still spread over the part.
+enum class ProjShape { k256x256, k256x128, k128x128 };
+
+static long tiles_of(long M, long N, long BN, long BM) { return ((M + BM - 1) / BM) * ((N + BN - 1) / BN); }
+
+static ProjShape shape_of(long M, long N) {
+    if (tiles_of(M, N, 256, 256) >= 256) return ProjShape::k256x256;
+    if (tiles_of(M, N, 256, 128) >= 256) return ProjShape::k256x128;
+    return ProjShape::k128x128;
+}
 
 long project_tiles(long M, long N) {
-    return big_tiles(M, N) ? ((M + 255) / 256) * ((N + 255) / 256) : ((M + 127) / 128) * ((N + 127) / 128);
+    switch (shape_of(M, N)) {
+        case ProjShape::k256x256: return tiles_of(M, N, 256, 256);
+        case ProjShape::k256x128: return tiles_of(M, N, 256, 128);
+        default: return tiles_of(M, N, 128, 128);
+    }
 }
 
 tk_status launch_project(const ProjectParams& p, hipStream_t st) {
     const long launched = ((long)p.tiles + kXcdCount - 1) / kXcdCount * kXcdCount;
-    if (big_tiles(p.M, p.N))
-        hipLaunchKernelGGL((project_kernel<256, 256>), dim3((unsigned)launched), dim3(ProjTile<256, 256>::kThreads),
-                           0, st, p);
-    else
-        hipLaunchKernelGGL((project_kernel<128, 128>), dim3((unsigned)launched), dim3(ProjTile<128, 128>::kThreads),
-                           0, st, p);
+    const dim3 grid((unsigned)launched);
+    switch (shape_of(p.M, p.N)) {
+        case ProjShape::k256x256:
+            hipLaunchKernelGGL((project_kernel<256, 256>), grid, dim3(ProjTile<256, 256>::kThreads), 0, st, p);
+            break;
+        case ProjShape::k256x128:
+            hipLaunchKernelGGL((project_kernel<256, 128>), grid, dim3(ProjTile<256, 128>::kThreads), 0, st, p);
+            break;
+        default:
+            hipLaunchKernelGGL((project_kernel<128, 128>), grid, dim3(ProjTile<128, 128>::kThreads), 0, st, p);
+    }
     return hipGetLastError() == hipSuccess ? TK_OK : TK_ERR_HIP;
 }
 
