@@ -13,7 +13,7 @@
 //
 // The weight is passed transposed, Wt [n_heads * width, d_model] (one row per
 // output column), so both operands of the product are contiguous along
-// d_model, which must be a multiple of 32 (one k-tile). The tile computes C^T = Wt X^T: a lane of each 32x32 accumulator
+// d_model, which must be a multiple of 32 (one k-tile). The tile computes C^T = Wt X^T: a lane of each accumulator
 // then holds four consecutive output columns of one token, which become one
 // 8-byte store into the head-major output row.
 #include "tk_device.hpp"
@@ -58,10 +58,12 @@ __device__ __forceinline__ void wait_copies(bool next_in_flight) {
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
-// Each wave multiplies a 64-column x BM / 2-token block: per 16-wide k-step 2
-// weight and BM / 64 token operand reads from LDS feed 2 BM / 64 MFMAs. Tiles
-// come from HBM by global->LDS copies (no staging registers), issued two
-// k-tiles ahead into a three-stage ring.
+// Each wave multiplies a 64-column x BM / 2-token block. Tiles come from HBM by
+// global->LDS copies (no staging registers), issued two k-tiles ahead into a
+// three-stage ring. The 256 x 256 tiles run 16x16x32 products in a ping-pong
+// between the two waves of each SIMD; the smaller ones run 32x32x16 products,
+// each wave reading the next 16-wide k-step's operands during the current one's
+// products.
 template <int BN>
 constexpr int proj_threads() { return 64 * (BN / 64) * 2; }
 
@@ -82,7 +84,6 @@ __global__ __launch_bounds__(proj_threads<BN>(), 1) void project_kernel(const Pr
     if (logical >= p.tiles) return;
     const int n_tiles = (p.N + kPBN - 1) / kPBN;
     const int n_base = (logical % n_tiles) * kPBN, m_base = (logical / n_tiles) * kPBM;
-    const int col = lane & 31, half = lane >> 5;
 
     // Copy i of this lane fills LDS slot i * 256 + tid of the tile: row slot / 4,
     // chunk (slot % 4) ^ ((row / 4) % 4) of that row in the matrix. Rows past the
@@ -111,82 +112,166 @@ __global__ __launch_bounds__(proj_threads<BN>(), 1) void project_kernel(const Pr
         for (int i = 0; i < kXCopies; ++i) copy16_to_lds(xk, xoff[i], sm.x[stage] + (i * kPThreads + wave * 64) * 8);
     };
 
-    f32x16 acc[2][T::kMB];
+    if constexpr (BM == 256) {
+        // ---- 256 x 256 tiles: ping-pong over the two waves of each SIMD ----
+        // The eight waves form two groups of four, one wave of each on every SIMD;
+        // the second group runs one barrier behind the first. A wave reads a whole
+        // k-tile's operands while the other wave of its SIMD runs its products, then
+        // runs its own products (32 of 16x16x32) while the other reads: the two
+        // phases alternate at every barrier. Each lane's 16-byte operand read is row
+        // r16 of a 16-row block at chunk q4, the whole 32-wide k-tile over the four
+        // lane groups, and an accumulator lane ends with four consecutive output
+        // columns of one token. Both groups pass 2 nk + 2 barriers: the late group's
+        // extra one comes first, the early group's last.
+        constexpr int kNB = BM / 32;
+        const int r16 = lane & 15, q4 = lane >> 4;
+        f32x4 acc[4][kNB];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < T::kMB; ++j)
+            for (int j = 0; j < kNB; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
-
-    const int nk = p.K / kPBK;
-    // operand reads of k-step ks of the k-tile in `st`, and the products of one k-step
-    auto read_ops = [&](int st, int ks, bf16x8 (&a)[2], bf16x8 (&b)[T::kMB]) {
-        const uint16_t* ws = sm.w[st];
-        const uint16_t* xs = sm.x[st];
-        const int kc = 2 * ks + half;
+                for (int v = 0; v < 4; ++v) acc[i][j][v] = 0.f;
+        const int nk = p.K / kPBK;
+        issue(0, 0);
+        if (nk > 1) issue(1, 1);
+        wait_copies<T::kCopies>(nk > 1);
+        __syncthreads();
+        const bool late = wave >= 4;
+        if (late) {
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+            __builtin_amdgcn_sched_barrier(0);
+        }
+        bf16x8 a[4], b[kNB];
+        int stage = 0;
+        for (int kt = 0; kt < nk; ++kt) {
+            // the stage k-tile kt + 2 goes to held k-tile kt - 1, which both groups
+            // have read before the barrier that opened this wave's read phase
+            const bool ahead = kt + 2 < nk;
+            if (ahead) issue(kt + 2, stage == 0 ? 2 : stage - 1);
+            const uint16_t* ws = sm.w[stage];
+            const uint16_t* xs = sm.x[stage];
 #pragma unroll
-        for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(ws + sw(wn * 64 + i * 32 + col, kc));
+            for (int i = 0; i < 4; ++i) a[i] = *(const bf16x8*)(ws + sw(wn * 64 + i * 16 + r16, q4));
 #pragma unroll
-        for (int j = 0; j < T::kMB; ++j) b[j] = *(const bf16x8*)(xs + sw(wm * (BM / 2) + j * 32 + col, kc));
-    };
-    auto products = [&](const bf16x8 (&a)[2], const bf16x8 (&b)[T::kMB]) {
+            for (int j = 0; j < kNB; ++j) b[j] = *(const bf16x8*)(xs + sw(wm * (BM / 2) + j * 16 + r16, q4));
+            wait_copies<T::kCopies>(ahead);  // k-tile kt + 1 has landed before the next barrier
+            // the schedule barriers keep the reads and products in their phases
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < kNB; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+            __builtin_amdgcn_sched_barrier(0);
+            stage = stage == kStages - 1 ? 0 : stage + 1;
+        }
+        if (!late) {
+            __builtin_amdgcn_sched_barrier(0);
+            __syncthreads();
+            __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int j = 0; j < kNB; ++j) {
+            const int m = m_base + wm * (BM / 2) + j * 16 + r16;
+            if (m >= p.M) continue;
+            const int bb = m / p.S, s = m - bb * p.S;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int n = n_base + wn * 64 + i * 16 + 4 * q4;
+                if (n >= p.N) continue;
+                const int h = n / p.width, w = n - h * p.width;
+                uint2 v;
+                v.x = pack_bf16(acc[i][j][0], acc[i][j][1]);
+                v.y = pack_bf16(acc[i][j][2], acc[i][j][3]);
+                *(uint2*)((uint16_t*)p.y + (((size_t)bb * p.heads + h) * p.S + s) * p.width + w) = v;
+            }
+        }
+    } else {
+        // ---- smaller tiles: 32x32x16 products, software-pipelined over k-steps ----
+        const int col = lane & 31, half = lane >> 5;
+        f32x16 acc[2][T::kMB];
 #pragma unroll
         for (int i = 0; i < 2; ++i)
 #pragma unroll
             for (int j = 0; j < T::kMB; ++j)
-                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    };
-    issue(0, 0);
-    if (nk > 1) issue(1, 1);
-    wait_copies<T::kCopies>(nk > 1);  // this lane's copies of k-tile 0 have landed
-    __syncthreads();      // ... and everyone's
-    static_assert(kPBK == 32, "the pipeline below takes two 16-wide k-steps per k-tile");
-    // Software pipeline over the k-steps: the operands of the next k-step are
-    // read while the current one's products run, and the barrier that publishes
-    // k-tile kt + 1 sits between the two k-steps of k-tile kt, so that its first
-    // operand reads overlap the second k-step's products.
-    bf16x8 a0[2], b0[T::kMB], a1[2], b1[T::kMB];
-    read_ops(0, 0, a0, b0);
-    int stage = 0;
-    for (int kt = 0; kt + 1 < nk; ++kt) {
-        // the stage k-tile kt + 2 goes to was last read before the barrier that
-        // ended iteration kt - 1
-        const bool ahead = kt + 2 < nk;
-        if (ahead) issue(kt + 2, stage == 0 ? 2 : stage - 1);
+#pragma unroll
+                for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+
+        const int nk = p.K / kPBK;
+        // operand reads of k-step ks of the k-tile in `st`, and the products of one k-step
+        auto read_ops = [&](int st, int ks, bf16x8 (&a)[2], bf16x8 (&b)[T::kMB]) {
+            const uint16_t* ws = sm.w[st];
+            const uint16_t* xs = sm.x[st];
+            const int kc = 2 * ks + half;
+#pragma unroll
+            for (int i = 0; i < 2; ++i) a[i] = *(const bf16x8*)(ws + sw(wn * 64 + i * 32 + col, kc));
+#pragma unroll
+            for (int j = 0; j < T::kMB; ++j) b[j] = *(const bf16x8*)(xs + sw(wm * (BM / 2) + j * 32 + col, kc));
+        };
+        auto products = [&](const bf16x8 (&a)[2], const bf16x8 (&b)[T::kMB]) {
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+#pragma unroll
+                for (int j = 0; j < T::kMB; ++j)
+                    acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+        };
+        issue(0, 0);
+        if (nk > 1) issue(1, 1);
+        wait_copies<T::kCopies>(nk > 1);  // this lane's copies of k-tile 0 have landed
+        __syncthreads();      // ... and everyone's
+        static_assert(kPBK == 32, "the pipeline below takes two 16-wide k-steps per k-tile");
+        // Software pipeline over the k-steps: the operands of the next k-step are
+        // read while the current one's products run, and the barrier that publishes
+        // k-tile kt + 1 sits between the two k-steps of k-tile kt, so that its first
+        // operand reads overlap the second k-step's products.
+        bf16x8 a0[2], b0[T::kMB], a1[2], b1[T::kMB];
+        read_ops(0, 0, a0, b0);
+        int stage = 0;
+        for (int kt = 0; kt + 1 < nk; ++kt) {
+            // the stage k-tile kt + 2 goes to was last read before the barrier that
+            // ended iteration kt - 1
+            const bool ahead = kt + 2 < nk;
+            if (ahead) issue(kt + 2, stage == 0 ? 2 : stage - 1);
+            read_ops(stage, 1, a1, b1);
+            products(a0, b0);
+            const int next = stage == kStages - 1 ? 0 : stage + 1;
+            wait_copies<T::kCopies>(ahead);  // k-tile kt + 1 has landed (kt + 2 may still fly)
+            __syncthreads();
+            read_ops(next, 0, a0, b0);
+            products(a1, b1);
+            stage = next;
+        }
+        // the last k-tile
         read_ops(stage, 1, a1, b1);
         products(a0, b0);
-        const int next = stage == kStages - 1 ? 0 : stage + 1;
-        wait_copies<T::kCopies>(ahead);  // k-tile kt + 1 has landed (kt + 2 may still fly)
-        __syncthreads();
-        read_ops(next, 0, a0, b0);
         products(a1, b1);
-        stage = next;
-    }
-    // the last k-tile
-    read_ops(stage, 1, a1, b1);
-    products(a0, b0);
-    products(a1, b1);
 
-    // ---- epilogue: lane (col, half) of block (i, j) holds output columns
-    // n0 + 8 g + 4 half + 0..3 (g = 0..3) of token m0 + col, rounded to bf16 and
-    // stored as 8 bytes into Y[b, h, s, w .. w + 3]
+        // ---- epilogue: lane (col, half) of block (i, j) holds output columns
+        // n0 + 8 g + 4 half + 0..3 (g = 0..3) of token m0 + col, rounded to bf16 and
+        // stored as 8 bytes into Y[b, h, s, w .. w + 3]
 #pragma unroll
-    for (int j = 0; j < T::kMB; ++j) {
-        const int m = m_base + wm * (BM / 2) + j * 32 + col;
-        if (m >= p.M) continue;
-        const int bb = m / p.S, s = m - bb * p.S;
+        for (int j = 0; j < T::kMB; ++j) {
+            const int m = m_base + wm * (BM / 2) + j * 32 + col;
+            if (m >= p.M) continue;
+            const int bb = m / p.S, s = m - bb * p.S;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+            for (int i = 0; i < 2; ++i) {
 #pragma unroll
-            for (int g = 0; g < 4; ++g) {
-                const int n = n_base + wn * 64 + i * 32 + 8 * g + 4 * half;
-                if (n >= p.N) continue;
-                const int h = n / p.width, w = n - h * p.width;
-                uint2 v;
-                v.x = pack_bf16(acc[i][j][4 * g], acc[i][j][4 * g + 1]);
-                v.y = pack_bf16(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
-                *(uint2*)((uint16_t*)p.y + (((size_t)bb * p.heads + h) * p.S + s) * p.width + w) = v;
+                for (int g = 0; g < 4; ++g) {
+                    const int n = n_base + wn * 64 + i * 32 + 8 * g + 4 * half;
+                    if (n >= p.N) continue;
+                    const int h = n / p.width, w = n - h * p.width;
+                    uint2 v;
+                    v.x = pack_bf16(acc[i][j][4 * g], acc[i][j][4 * g + 1]);
+                    v.y = pack_bf16(acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
+                    *(uint2*)((uint16_t*)p.y + (((size_t)bb * p.heads + h) * p.S + s) * p.width + w) = v;
+                }
             }
         }
     }

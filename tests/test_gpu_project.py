@@ -57,6 +57,8 @@ SHAPES = [  # (B, S, d_model, heads, width)
     (1, 129, 160, 3, 20),     # an odd number of 32-wide k-tiles, 60 columns, ragged tokens
     (2, 2048, 1024, 32, 128),  # 256 x 256 workgroup tiles (at least one per CU)
     (1, 4100, 256, 64, 68),   # 256 x 256 tiles with tails in tokens and columns
+    (1, 4100, 160, 64, 68),   # 256 x 256 tiles over an odd number (5) of k-tiles
+    (1, 4096, 32, 64, 64),    # 256 x 256 tiles over a single k-tile
     (2, 16350, 288, 7, 36),   # 256 x 128 tiles (narrow and long): ragged columns and tokens, 9 k-tiles
 ]
 
